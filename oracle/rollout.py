@@ -1,0 +1,166 @@
+"""Oracle: cached rollout G_tau(c, s), scorer and CachedSearch exploration.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+Follows the paper step by step, in float64:
+
+* Euler step of the probability-flow ODE on the decreasing grid
+  t_1 = 1 > ... > t_{T+1} = 0 (Sec. Preliminaries, Eq. euler);
+* classifier-free guidance v_u + w (v_c - v_u) (Eq. cfg), one transformer
+  call per guidance branch;
+* the transformation-vector cache (Sec. Adaptive transformation-vector
+  caching): a computed call stores Delta = v(x_ref) - x_ref (Eq. delta) and
+  x_ref; a skipped call returns x + Delta (Eq. skip);
+* the accumulated drift indicator a += ||x - x_ref|| / ||x_ref|| (Eq.
+  indicator): skip while a <= tau, otherwise compute, refresh Delta and
+  x_ref and reset a to 0; the first K_w and last K_c steps, and any call
+  before the first Delta exists, always compute;
+* independent (Delta, x_ref, a) per guidance branch (Sec. per-branch cache
+  state), reset at the start of every generation (Alg. 1);
+* the static variant that computes every k-th step between warmup and
+  cooldown (Sec. properties);
+* the scorer, a fixed random projection s = <w, x_{T+1}> / sqrt(D), which
+  stands in for the verifier V of Alg. 1.
+
+Readings where the paper is silent:
+  - steps are 1-based; steps 1..K_w and T-K_c+1..T are forced computes;
+  - every computed call (forced or not) refreshes Delta, x_ref and resets a;
+    a forced step does not add to a;
+  - a call whose ||x_ref|| is 0 computes;
+  - both branches receive the latent x_{t_k} of the current step;
+  - static mode with period k computes a step s (K_w < s <= T-K_c) iff
+    (s - K_w) is a multiple of k; other steps in that range reuse Delta.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Callable, Dict, List, Optional, Sequence
+
+import numpy as np
+
+from . import dit
+
+CACHE_OFF, CACHE_ADAPTIVE, CACHE_STATIC = 0, 1, 2
+
+
+@dataclasses.dataclass
+class StepRecord:
+    """One cache decision: step k (1-based), candidate i, branch b,
+    ``a`` = the indicator compared with tau (None on a forced step), and
+    ``compute`` = whether the transformer was evaluated."""
+    k: int
+    i: int
+    b: int
+    a: Optional[float]
+    compute: bool
+
+
+@dataclasses.dataclass
+class RolloutResult:
+    latents: np.ndarray          # [N][C][F][H][W] float64, x_{T+1}
+    log: List[StepRecord]
+    n_compute: int
+    n_calls: int
+
+    def schedule(self, i: int, b: int) -> List[bool]:
+        return [r.compute for r in self.log if r.i == i and r.b == b]
+
+    def a_values(self, i: int, b: int) -> List[Optional[float]]:
+        return [r.a for r in self.log if r.i == i and r.b == b]
+
+
+def is_forced(k: int, T: int, k_warm: int, k_cool: int, has_ref: bool, mode: int) -> bool:
+    return (mode == CACHE_OFF) or (k <= k_warm) or (k > T - k_cool) or (not has_ref)
+
+
+def cached_rollout_one(x1: np.ndarray, velocity_fns: Sequence[Callable[[np.ndarray, float], np.ndarray]],
+                       timesteps: Sequence[float], *, tau: float, k_warm: int, k_cool: int,
+                       guidance: float, mode: int = CACHE_ADAPTIVE, static_k: int = 2,
+                       cand: int = 0, log: Optional[List[StepRecord]] = None) -> np.ndarray:
+    """One candidate's rollout.  ``velocity_fns[b](x, t)`` is the transformer
+    call of guidance branch b (b = 0 conditional, b = 1 unconditional)."""
+    B = len(velocity_fns)
+    T = len(timesteps) - 1
+    x = dit.as64(x1).copy()
+    # cache state per branch, reset at the start of the generation (Alg. 1)
+    has_ref = [False] * B
+    a = [0.0] * B
+    xref: List[Optional[np.ndarray]] = [None] * B
+    delta: List[Optional[np.ndarray]] = [None] * B
+    for k in range(1, T + 1):
+        t_k, t_next = float(timesteps[k - 1]), float(timesteps[k])
+        v = [None] * B
+        for b in range(B):
+            forced = is_forced(k, T, k_warm, k_cool, has_ref[b], mode)
+            compute = True
+            a_seen: Optional[float] = None
+            if not forced:
+                if mode == CACHE_STATIC:
+                    compute = ((k - k_warm) % static_k) == 0
+                else:
+                    num = math.sqrt(float(np.sum((x - xref[b]) ** 2)))
+                    den = math.sqrt(float(np.sum(xref[b] ** 2)))
+                    if den == 0.0:
+                        compute = True
+                    else:
+                        a[b] += num / den
+                        a_seen = a[b]
+                        compute = not (a[b] <= tau)
+            if compute:
+                v[b] = dit.as64(velocity_fns[b](x, t_k))
+                delta[b] = v[b] - x
+                xref[b] = x.copy()
+                a[b] = 0.0
+                has_ref[b] = True
+            else:
+                v[b] = x + delta[b]
+            if log is not None:
+                log.append(StepRecord(k, cand, b, a_seen, compute))
+        vt = v[0] if B == 1 else v[1] + guidance * (v[0] - v[1])
+        x = x + (t_next - t_k) * vt
+    return x
+
+
+def dit_velocity_fns(W: Dict[str, np.ndarray], cfg, ctx: Sequence[np.ndarray]):
+    """Transformer calls per guidance branch; the text embedding of each
+    branch's context is computed once per rollout (it depends on c only)."""
+    embs = [dit.text_embedding(c, W) for c in ctx]
+    return [(lambda x, t, e=e: dit.velocity(x, t, e, W, cfg)) for e in embs]
+
+
+def cached_rollout(x1: np.ndarray, velocity_fns, timesteps, *, tau: float, k_warm: int,
+                   k_cool: int, guidance: float = 5.0, mode: int = CACHE_ADAPTIVE,
+                   static_k: int = 2) -> RolloutResult:
+    """N independent candidate rollouts, x1 [N][...]."""
+    log: List[StepRecord] = []
+    outs = []
+    for i in range(x1.shape[0]):
+        outs.append(cached_rollout_one(x1[i], velocity_fns, timesteps, tau=tau, k_warm=k_warm,
+                                       k_cool=k_cool, guidance=guidance, mode=mode,
+                                       static_k=static_k, cand=i, log=log))
+    n_comp = sum(1 for r in log if r.compute)
+    return RolloutResult(np.stack(outs), log, n_comp, len(log))
+
+
+def score(latents: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """s_i = <w, x_i> / sqrt(D) for every candidate (float64)."""
+    X = dit.as64(latents).reshape(latents.shape[0], -1)
+    D = X.shape[1]
+    return (X @ dit.as64(w)) / math.sqrt(D)
+
+
+def run_workload(wl, *, tau: Optional[float] = None, mode: Optional[int] = None,
+                 n_cand: Optional[int] = None) -> RolloutResult:
+    """Oracle rollout of a synthetic workload (see ``synth.make_workload``)."""
+    from_cfg = wl.roll
+    W = {k: v.astype(np.float64) for k, v in wl.named_weights().items()}
+    fns = dit_velocity_fns(W, wl.model, wl.ctx[:from_cfg.n_branch])
+    x1 = wl.noise if n_cand is None else wl.noise[:n_cand]
+    return cached_rollout(x1, fns, [float(t) for t in wl.timesteps],
+                          tau=from_cfg.tau if tau is None else tau,
+                          k_warm=from_cfg.k_warm, k_cool=from_cfg.k_cool,
+                          guidance=from_cfg.guidance,
+                          mode=from_cfg.mode if mode is None else mode,
+                          static_k=from_cfg.static_k)
+
