@@ -1,0 +1,82 @@
+// Shared definitions for the gfx950 kernels and the runtime.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+#define CS_DEV __device__ __forceinline__
+
+constexpr int WAVE = 64;
+
+// ---------------------------------------------------------------------------
+// 32x32 MFMA family, per element type.
+//   A operand (32 x KSTEP): lane l holds row l%32, k = KPL*(l/32) + i.
+//   B operand (KSTEP x 32): lane l holds column l%32, k = KPL*(l/32) + i.
+//   Accumulator (32 x 32, 16 floats): register j of lane l is
+//     row 8*(j/4) + 4*(l/32) + (j%4), column l%32.
+// bf16: v_mfma_f32_32x32x16_bf16 (8 values per lane, K = 16).
+// fp32: v_mfma_f32_32x32x2_f32   (1 value per lane,  K = 2).
+// ---------------------------------------------------------------------------
+template <typename T> struct Mfma32;
+
+template <> struct Mfma32<bf16> {
+  static constexpr int KPL = 8;
+  static constexpr int KSTEP = 16;
+  typedef bf16x8 frag;
+  static CS_DEV f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  static CS_DEV frag load(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+};
+
+template <> struct Mfma32<float> {
+  static constexpr int KPL = 1;
+  static constexpr int KSTEP = 2;
+  typedef float frag;
+  static CS_DEV f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  static CS_DEV frag load(const float* p) { return *p; }
+};
+
+// Accumulator register j -> row offset inside the 32x32 tile for lane l.
+CS_DEV int acc_row(int j, int lane) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
+
+template <typename T> CS_DEV T to_t(float v);
+template <> CS_DEV bf16 to_t<bf16>(float v) { return (bf16)v; }
+template <> CS_DEV float to_t<float>(float v) { return v; }
+template <typename T> CS_DEV float to_f(T v) { return (float)v; }
+
+// 16-byte copy helpers.
+struct alignas(16) Chunk16 { uint32_t w[4]; };
+CS_DEV Chunk16 ld16(const void* p) { return *reinterpret_cast<const Chunk16*>(p); }
+CS_DEV void st16(void* p, Chunk16 c) { *reinterpret_cast<Chunk16*>(p) = c; }
+
+CS_DEV float gelu_tanh(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  float u = k0 * (x + 0.044715f * x * x * x);
+  return 0.5f * x * (1.0f + tanhf(u));
+}
+CS_DEV float silu(float x) { return x / (1.0f + expf(-x)); }
+
+CS_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  return v;
+}
+CS_DEV double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  return v;
+}
+
+inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+inline long round_up(long a, long b) { return (a + b - 1) / b * b; }

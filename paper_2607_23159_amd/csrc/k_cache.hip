@@ -1,0 +1,236 @@
+// Cache rule, fused skip/refresh/CFG/Euler update, and score reduction.
+//
+// Decision (Eq. indicator): per stream s = (candidate i, branch b) the drift
+// ||x_i - xref_s||_F / ||xref_s||_F is accumulated into a_s; the call is
+// skipped iff a_s <= tau, else it computes and a_s resets to 0.  The two
+// sums are reduced in fp64, first per (candidate, 8192-element chunk) by a
+// coalesced streaming kernel that reads x once for all branches, then per
+// stream in chunk order by a one-wave kernel that also compacts the list of
+// computing streams with a ballot (no atomics: results do not depend on
+// timing).
+//
+// Update: skipped streams use x + Delta (Eq. skip); computed streams take
+// the transformer output v and, when the cache is on, refresh Delta = v - x
+// and xref = x (Eq. delta); branches are combined by Eq. cfg and the Euler
+// step of Eq. euler is applied, all in one pass over the latents.
+#include "kernels.hpp"
+
+namespace cs {
+
+constexpr int CHUNK_F4 = 8;                     // float4 per thread per chunk
+constexpr int CHUNK = 256 * 4 * CHUNK_F4;       // 8192 elements
+
+int decide_chunks(long D) { return cdiv(D, CHUNK); }
+int score_chunks(long D) { return cdiv(D, CHUNK); }
+
+// Block-wide fp64 sum in a fixed order (wave sums, then waves in order).
+__device__ double block_sum(double v, double* sh) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sh[wave] = v;
+  __syncthreads();
+  double t = 0.0;
+  if (threadIdx.x == 0) t = ((sh[0] + sh[1]) + sh[2]) + sh[3];
+  return t;
+}
+
+__global__ __launch_bounds__(256) void k_decide_partials(const float* __restrict__ x,
+                                                          const float* __restrict__ xref,
+                                                          int n_branch, long D,
+                                                          double* __restrict__ partials) {
+  __shared__ double sh[4];
+  const int chunk = blockIdx.x, nchunk = gridDim.x, i = blockIdx.y;
+  const long D4 = D >> 2;
+  const float4* xi = reinterpret_cast<const float4*>(x + (long)i * D);
+  double num[2] = {0.0, 0.0}, den[2] = {0.0, 0.0};
+  for (int k = 0; k < CHUNK_F4; ++k) {
+    const long j = (long)chunk * (CHUNK / 4) + k * 256 + threadIdx.x;
+    if (j < D4) {
+      const float4 xv = xi[j];
+      for (int b = 0; b < n_branch; ++b) {
+        const float4 r = reinterpret_cast<const float4*>(xref + ((long)i * n_branch + b) * D)[j];
+        const float d0 = xv.x - r.x, d1 = xv.y - r.y, d2 = xv.z - r.z, d3 = xv.w - r.w;
+        num[b] += ((double)d0 * d0 + (double)d1 * d1) + ((double)d2 * d2 + (double)d3 * d3);
+        den[b] += ((double)r.x * r.x + (double)r.y * r.y) + ((double)r.z * r.z + (double)r.w * r.w);
+      }
+    }
+  }
+  for (int b = 0; b < n_branch; ++b) {
+    const double tn = block_sum(num[b], sh);
+    const double td = block_sum(den[b], sh);
+    if (threadIdx.x == 0) {
+      double* p = partials + (((long)i * n_branch + b) * nchunk + chunk) * 2;
+      p[0] = tn;
+      p[1] = td;
+    }
+  }
+}
+
+hipError_t decide_partials(const float* x, const float* xref, int n_cand, int n_branch, long D,
+                           double* partials, hipStream_t st) {
+  dim3 grid((unsigned)decide_chunks(D), (unsigned)n_cand);
+  hipLaunchKernelGGL(k_decide_partials, grid, dim3(256), 0, st, x, xref, n_branch, D, partials);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(64) void k_decide_finalize(DecideParams p,
+                                                         const double* __restrict__ partials,
+                                                         const uint8_t* __restrict__ ovr,
+                                                         double* __restrict__ a,
+                                                         uint8_t* __restrict__ has_ref,
+                                                         uint8_t* __restrict__ mask,
+                                                         double* __restrict__ a_seen,
+                                                         int32_t* __restrict__ slots,
+                                                         int32_t* __restrict__ branch,
+                                                         DecideOut* __restrict__ out) {
+  const int lane = threadIdx.x;
+  int count = 0;
+  for (int base = 0; base < p.n_streams; base += 64) {
+    const int s = base + lane;
+    const bool valid = s < p.n_streams;
+    bool compute = true;
+    if (valid) {
+      const bool forced = p.mode == 0 || p.step <= p.k_warm || p.step > p.n_steps - p.k_cool ||
+                          !has_ref[s];
+      double seen = __builtin_nan("");
+      if (!forced) {
+        if (p.mode == 2) {
+          compute = ((p.step - p.k_warm) % p.static_k) == 0;
+        } else if (p.use_partials) {
+          double num = 0.0, den = 0.0;
+          const double* ps = partials + (long)s * p.nchunk * 2;
+          for (int c = 0; c < p.nchunk; ++c) {
+            num += ps[2 * c];
+            den += ps[2 * c + 1];
+          }
+          if (den > 0.0) {
+            a[s] += sqrt(num) / sqrt(den);
+            seen = a[s];
+            compute = !(a[s] <= p.tau);
+          }
+        }
+      }
+      if (p.use_override) compute = ovr[s] != 0;
+      if (compute) {
+        a[s] = 0.0;
+        has_ref[s] = 1;
+      }
+      mask[s] = compute ? 1 : 0;
+      a_seen[s] = seen;
+    }
+    const unsigned long long bal = __ballot(valid && compute);
+    const unsigned long long below = lane == 0 ? 0ull : (bal & ((1ull << lane) - 1ull));
+    if (valid && compute) {
+      slots[count + __popcll(below)] = s;
+      branch[count + __popcll(below)] = s % p.n_branch;
+    }
+    count += __popcll(bal);
+  }
+  if (lane == 0) out->n_compute = count;
+}
+
+hipError_t decide_finalize(const DecideParams& p, const double* partials, const uint8_t* ovr,
+                           double* a, uint8_t* has_ref, uint8_t* mask, double* a_seen,
+                           int32_t* slots, int32_t* branch, DecideOut* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_decide_finalize, dim3(1), dim3(64), 0, st, p, partials, ovr, a, has_ref,
+                     mask, a_seen, slots, branch, out);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_cache_update(float* __restrict__ x, float* __restrict__ xref,
+                                                       float* __restrict__ delta,
+                                                       const float* __restrict__ vbuf,
+                                                       const uint8_t* __restrict__ mask, int n_cand,
+                                                       int n_branch, long D, float dt, float w,
+                                                       int store_state) {
+  const long D4 = D >> 2;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)n_cand * D4) return;
+  const int i = (int)(idx / D4);
+  const long j = idx - (long)i * D4;
+  float4* xp = reinterpret_cast<float4*>(x + (long)i * D) + j;
+  const float4 xv = *xp;
+  float4 v[2];
+  for (int b = 0; b < n_branch; ++b) {
+    const long s = (long)i * n_branch + b;
+    float4* dp = reinterpret_cast<float4*>(delta + s * D) + j;
+    if (mask[s]) {
+      const float4 vb = reinterpret_cast<const float4*>(vbuf + s * D)[j];
+      if (store_state) {
+        float4 dv;
+        dv.x = vb.x - xv.x; dv.y = vb.y - xv.y; dv.z = vb.z - xv.z; dv.w = vb.w - xv.w;
+        *dp = dv;
+        reinterpret_cast<float4*>(xref + s * D)[j] = xv;
+      }
+      v[b] = vb;
+    } else {
+      const float4 dv = *dp;
+      v[b].x = xv.x + dv.x; v[b].y = xv.y + dv.y; v[b].z = xv.z + dv.z; v[b].w = xv.w + dv.w;
+    }
+  }
+  float4 vt = v[0];
+  if (n_branch == 2) {
+    vt.x = v[1].x + w * (v[0].x - v[1].x);
+    vt.y = v[1].y + w * (v[0].y - v[1].y);
+    vt.z = v[1].z + w * (v[0].z - v[1].z);
+    vt.w = v[1].w + w * (v[0].w - v[1].w);
+  }
+  float4 xn;
+  xn.x = xv.x + dt * vt.x; xn.y = xv.y + dt * vt.y; xn.z = xv.z + dt * vt.z; xn.w = xv.w + dt * vt.w;
+  *xp = xn;
+}
+
+hipError_t cache_update(float* x, float* xref, float* delta, const float* vbuf, const uint8_t* mask,
+                        int n_cand, int n_branch, long D, float dt, float guidance,
+                        int store_state, hipStream_t st) {
+  const long n = (long)n_cand * (D >> 2);
+  hipLaunchKernelGGL(k_cache_update, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, x, xref, delta,
+                     vbuf, mask, n_cand, n_branch, D, dt, guidance, store_state);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_score_partials(const float* __restrict__ x,
+                                                         const float* __restrict__ w, long D,
+                                                         double* __restrict__ partials) {
+  __shared__ double sh[4];
+  const int chunk = blockIdx.x, nchunk = gridDim.x, i = blockIdx.y;
+  const long D4 = D >> 2;
+  const float4* xi = reinterpret_cast<const float4*>(x + (long)i * D);
+  const float4* wv = reinterpret_cast<const float4*>(w);
+  double acc = 0.0;
+  for (int k = 0; k < CHUNK_F4; ++k) {
+    const long j = (long)chunk * (CHUNK / 4) + k * 256 + threadIdx.x;
+    if (j < D4) {
+      const float4 a = xi[j], b = wv[j];
+      acc += ((double)a.x * b.x + (double)a.y * b.y) + ((double)a.z * b.z + (double)a.w * b.w);
+    }
+  }
+  const double t = block_sum(acc, sh);
+  if (threadIdx.x == 0) partials[(long)i * nchunk + chunk] = t;
+}
+
+hipError_t score_partials(const float* x, const float* w, int n_cand, long D, double* partials,
+                          hipStream_t st) {
+  dim3 grid((unsigned)score_chunks(D), (unsigned)n_cand);
+  hipLaunchKernelGGL(k_score_partials, grid, dim3(256), 0, st, x, w, D, partials);
+  return hipGetLastError();
+}
+
+__global__ void k_score_finalize(const double* __restrict__ partials, int n_cand, int nchunk,
+                                 double inv_sqrt_d, double* __restrict__ scores) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_cand) return;
+  double s = 0.0;
+  for (int c = 0; c < nchunk; ++c) s += partials[(long)i * nchunk + c];
+  scores[i] = s * inv_sqrt_d;
+}
+
+hipError_t score_finalize(const double* partials, int n_cand, int nchunk, long D, double* scores,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)cdiv(n_cand, 64)), dim3(64), 0, st, partials,
+                     n_cand, nchunk, 1.0 / sqrt((double)D), scores);
+  return hipGetLastError();
+}
+
+}  // namespace cs

@@ -1,0 +1,264 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle.
+
+Velocity parity per model shape (tiny, Wan widths at 384 tokens, one
+Wan2.1-1.3B block at the full 32,760 tokens on sampled tokens), rollout
+parity (schedules, latents, scores, rankings) on the tiny workload for
+fp32 and bf16, one and two guidance branches and tau in
+{0, 0.05, 0.1, 0.2, inf}, and a Wan-width rollout."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from oracle import dit as odit
+from oracle import rank as orank
+from oracle import rollout as orl
+from paper_2607_23159_amd import synth
+from paper_2607_23159_amd import binding as B
+from paper_2607_23159_amd.search import GpuModel, Inputs, run_rollout
+from parity import TOL, compare_schedules, oracle_masks, rel_l2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+_models = {}
+
+
+def gpu_model(name, dtype, init):
+    key = (name, dtype, init)
+    if key not in _models:
+        m = synth.MODELS[name].with_dtype(dtype)
+        _models[key] = (GpuModel(m, synth.make_weights(m, init=init)), m)
+    return _models[key]
+
+
+def oracle_weights(m, init):
+    return {k: v.astype(np.float64) for k, v in synth.unflatten(m, synth.make_weights(m, init=init)).items()}
+
+
+# ----------------------------------------------------------------- velocity
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
+@pytest.mark.parametrize("init", ["paper", "stress"])
+def test_velocity_tiny(dtype, init):
+    say(f"velocity tiny dtype={dtype} init={init}")
+    gm, m = gpu_model("tiny", dtype, init)
+    W = oracle_weights(m, init)
+    x = synth.make_noise(m, 3, seed0=500)
+    ctx = synth.make_context(m, 1)
+    for t in (1.0, 0.55, 0.05):
+        v = gm.velocity(torch.from_numpy(x.reshape(3, -1)).cuda(), t, torch.from_numpy(ctx).cuda())
+        v = v.cpu().numpy().reshape(x.shape)
+        emb = odit.text_embedding(ctx, W)
+        for i in range(3):
+            ref = odit.velocity(x[i], t, emb, W, m)
+            err = rel_l2(v[i], ref)
+            say(f"  t={t} i={i} rel_l2={err:.3e}")
+            assert err < TOL[dtype] / 4
+
+
+@pytest.mark.parametrize("init", ["paper", "stress"])
+def test_velocity_wan_mid_bf16(init):
+    say(f"velocity wan_mid bf16 init={init}")
+    gm, m = gpu_model("wan_mid", synth.DTYPE_BF16, init)
+    W = oracle_weights(m, init)
+    x = synth.make_noise(m, 2, seed0=600)
+    ctx = synth.make_context(m, 1)
+    v = gm.velocity(torch.from_numpy(x.reshape(2, -1)).cuda(), 0.7, torch.from_numpy(ctx).cuda())
+    v = v.cpu().numpy().reshape(x.shape)
+    emb = odit.text_embedding(ctx, W)
+    for i in range(2):
+        err = rel_l2(v[i], odit.velocity(x[i], 0.7, emb, W, m))
+        say(f"  i={i} rel_l2={err:.3e}")
+        assert err < TOL[0] / 2
+
+
+def test_velocity_full_length_block_sampled():
+    """One Wan2.1-1.3B block at 32,760 tokens (ragged last key tile, 256-row
+    GEMM tail), checked on sampled tokens."""
+    say("velocity wan13b_block1 bf16 full length, sampled tokens")
+    gm, m = gpu_model("wan13b_block1", synth.DTYPE_BF16, "stress")
+    W = oracle_weights(m, "stress")
+    x = synth.make_noise(m, 1, seed0=700)
+    ctx = synth.make_context(m, 1)
+    v = gm.velocity(torch.from_numpy(x.reshape(1, -1)).cuda(), 0.8, torch.from_numpy(ctx).cuda())
+    vp = odit.patchify(v.cpu().numpy().reshape(x.shape[1:]), 1, 2, 2)
+    rows = np.array([0, 1, 63, 255, 256, 4097, 16383, 32511, 32512, 32700, 32759])
+    ref = odit.velocity(x[0], 0.8, odit.text_embedding(ctx, W), W, m, last_block_rows=rows)
+    err = rel_l2(vp[rows], ref)
+    say(f"  sampled rel_l2={err:.3e}")
+    assert err < TOL[0] / 2
+
+
+def test_batch_invariance_velocity():
+    """A latent's velocity is bitwise the same alone or inside a batch."""
+    gm, m = gpu_model("tiny", synth.DTYPE_BF16, "stress")
+    x = torch.from_numpy(synth.make_noise(m, 5, seed0=800).reshape(5, -1)).cuda()
+    ctx = torch.from_numpy(synth.make_context(m, 1)).cuda()
+    full = gm.velocity(x, 0.4, ctx)
+    for i in (0, 2, 4):
+        one = gm.velocity(x[i:i + 1].contiguous(), 0.4, ctx)
+        assert torch.equal(one[0], full[i])
+    two = gm.velocity(x[1:3].contiguous(), 0.4, ctx)
+    assert torch.equal(two, full[1:3])
+
+
+# ------------------------------------------------------------------ rollouts
+_oracle_cache = {}
+
+
+def oracle_rollout(wl, tau, mode=None, key=None):
+    k = (key, tau, mode)
+    if k not in _oracle_cache:
+        _oracle_cache[k] = orl.run_workload(wl, tau=tau, mode=mode)
+    return _oracle_cache[k]
+
+
+_wls = {}
+
+
+def workload(name, n_branch, init, dtype):
+    k = (name, n_branch, init, dtype)
+    if k not in _wls:
+        _wls[k] = synth.make_workload(name, n_branch=n_branch, init=init, dtype=dtype)
+    return _wls[k]
+
+
+def check_rollout(gm, wl, tau, dtype, okey):
+    r = wl.roll
+    res = oracle_rollout(wl, tau, key=okey)
+    om, oa = oracle_masks(res, r.n_cand, r.n_branch, r.n_steps)
+    g = run_rollout(gm, wl, tau=tau)
+    excused = compare_schedules(g.masks, om, oa, tau)
+    say(f"  tau={tau} computed gpu {g.computed}/{g.calls} oracle {res.n_compute}/{res.n_calls} excused={excused}")
+    if excused:
+        g = run_rollout(gm, wl, tau=tau, override=om)
+        assert np.array_equal(g.masks, om)
+    for i in range(r.n_cand):
+        err = rel_l2(g.latents[i], res.latents[i])
+        assert err < TOL[dtype], (i, err)
+    s_ref = orl.score(res.latents, wl.scorer)
+    np.testing.assert_allclose(g.scores, s_ref, rtol=0, atol=TOL[dtype] * np.abs(s_ref).max() + 1e-9)
+    # ranking: exact unless two oracle scores are closer than the score error
+    gap_tol = 4 * np.abs(g.scores - s_ref).max()
+    oo = orank.order_desc(list(s_ref))
+    og = orank.order_desc(list(g.scores))
+    if oo != og:
+        srt = np.sort(s_ref)
+        assert np.min(np.diff(srt)) <= gap_tol, (oo, og)
+    return g, res
+
+
+@pytest.mark.parametrize("n_branch", [1, 2])
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
+def test_rollout_tiny(dtype, n_branch):
+    say(f"rollout tiny dtype={dtype} B={n_branch}")
+    gm, m = gpu_model("tiny", dtype, "stress")
+    wl = workload("tiny", n_branch, "stress", dtype)
+    for tau in (0.0, 0.05, 0.1, 0.2, math.inf):
+        check_rollout(gm, wl, tau, dtype, okey=("tiny", n_branch))
+
+
+def test_rollout_wan_mid_bf16():
+    say("rollout wan_mid bf16 B=1 N=2")
+    gm, m = gpu_model("wan_mid", synth.DTYPE_BF16, "paper")
+    wl = synth.make_workload("wan_mid", n_branch=1, init="paper", n_cand=2)
+    g, res = check_rollout(gm, wl, 0.1, synth.DTYPE_BF16, okey=("wan_mid", 1))
+    assert 0 < res.n_compute < res.n_calls
+
+
+# ---------------------------------------------------------------- invariants
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
+def test_tau0_bitwise_equals_off(dtype):
+    gm, m = gpu_model("tiny", dtype, "stress")
+    wl = workload("tiny", 2, "stress", dtype)
+    a = run_rollout(gm, wl, tau=0.0)
+    b = run_rollout(gm, wl, mode=synth.CACHE_OFF)
+    assert a.computed == a.calls == b.computed
+    assert np.array_equal(a.latents, b.latents)
+    assert np.array_equal(a.scores, b.scores)
+
+
+def test_tau_inf_forced_only_and_branches_coincide():
+    gm, m = gpu_model("tiny", synth.DTYPE_BF16, "stress")
+    wl = workload("tiny", 2, "stress", synth.DTYPE_BF16)
+    g = run_rollout(gm, wl, tau=math.inf)
+    r = wl.roll
+    assert (g.masks.sum(axis=0) == r.k_warm + r.k_cool).all()
+    g = run_rollout(gm, wl, tau=0.1)
+    for i in range(r.n_cand):
+        assert np.array_equal(g.masks[:, 2 * i], g.masks[:, 2 * i + 1])
+
+
+def test_static_mode_schedule():
+    gm, m = gpu_model("tiny", synth.DTYPE_FP32, "stress")
+    wl = synth.make_workload("tiny", dtype=synth.DTYPE_FP32, init="stress", mode=synth.CACHE_STATIC,
+                             static_k=3, k_warm=2, k_cool=2)
+    g = run_rollout(gm, wl)
+    want = [1 if k in (1, 2, 5, 8, 9, 10) else 0 for k in range(1, 11)]
+    assert (g.masks == np.array(want, np.uint8)[:, None]).all()
+    res = orl.run_workload(wl)
+    for i in range(wl.roll.n_cand):
+        assert rel_l2(g.latents[i], res.latents[i]) < TOL[1]
+
+
+def test_replay_override_follows_given_schedule():
+    gm, m = gpu_model("tiny", synth.DTYPE_FP32, "stress")
+    wl = workload("tiny", 1, "stress", synth.DTYPE_FP32)
+    T, S = wl.roll.n_steps, wl.roll.n_cand
+    ovr = np.zeros((T, S), np.uint8)
+    ovr[0] = 1
+    ovr[4] = 1
+    ovr[8] = 1
+    ovr[-1] = 1
+    g = run_rollout(gm, wl, override=ovr)
+    assert np.array_equal(g.masks, ovr)
+    # the same schedule in the oracle (velocity calls replayed via STATIC-like mask)
+    W = {k: v.astype(np.float64) for k, v in wl.named_weights().items()}
+    fns = orl.dit_velocity_fns(W, wl.model, wl.ctx[:1])
+    # k_warm=1, k_cool=1, static period 4 computes steps 1, 5, 9, 10
+    res = orl.cached_rollout(wl.noise, fns, [float(t) for t in wl.timesteps], tau=0.0, k_warm=1, k_cool=1,
+                             guidance=5.0, mode=orl.CACHE_STATIC, static_k=4)
+    om, _ = oracle_masks(res, S, 1, T)
+    assert np.array_equal(om, ovr)
+    for i in range(S):
+        assert rel_l2(g.latents[i], res.latents[i]) < TOL[1]
+
+
+def test_checkpoint_resume_bitwise():
+    gm, m = gpu_model("tiny", synth.DTYPE_BF16, "stress")
+    wl = workload("tiny", 2, "stress", synth.DTYPE_BF16)
+    ref = run_rollout(gm, wl, tau=0.1, record=False)
+    inp = Inputs(wl)
+    r = wl.roll
+    desc = B.RolloutDesc(r, wl.timesteps, tau=0.1)
+    h = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[1])
+    for k in range(1, 5):
+        B.cs_denoise_step(h, k)
+    blob = B.cs_rollout_export(h)
+    B.cs_rollout_free(h)
+    h2 = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[1])
+    B.cs_rollout_import(h2, blob)
+    with pytest.raises(B.CsError) as e:
+        B.cs_denoise_step(h2, 4)
+    assert e.value.status == B.CS_E_STATE
+    for k in range(5, r.n_steps + 1):
+        B.cs_denoise_step(h2, k)
+    out = torch.empty_like(inp.x1)
+    B.cs_rollout_latents(h2, out)
+    torch.cuda.synchronize()
+    B.cs_rollout_free(h2)
+    assert np.array_equal(out.cpu().numpy().reshape(ref.latents.shape), ref.latents)
