@@ -1,0 +1,229 @@
+"""Benchmark: cached candidate denoise-steps/s on one MI355X.
+
+One step = one CachedSearch exploration pass (Alg. 1) over one batch of
+synthetic inputs: rollout init (cache reset, text keys/values), T Euler
+steps of N candidates with the cache decision, transformer on the computed
+calls, skip/refresh/CFG/Euler update, then scoring and ranking.  The
+full-compute reference rollout of the same seeds (cache off) is tau
+independent; with --reference it is run once before the timed region and
+the cached ranking is compared with it (Spearman rho, top-1).
+
+Printed: one JSON line with the metric, the roofline of the dominant kernel
+(self-attention, timed by HIP events on the rollout stream inside the
+library), and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=1)
+    p.add_argument("--warmup", type=int, default=0)
+    p.add_argument("--workload", default="wan13b_cached")
+    p.add_argument("--tau", type=float, default=None)
+    p.add_argument("--n-cand", type=int, default=None)
+    p.add_argument("--n-steps", type=int, default=None)
+    p.add_argument("--cfg", action="store_true", help="two guidance branches (w = 5.0)")
+    p.add_argument("--fp32", action="store_true", help="fp32 transformer arithmetic")
+    p.add_argument("--reference", action="store_true", help="also run the full rollouts for rho")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-profile", action="store_true", help="no per-kernel HIP event timing")
+    return p.parse_args()
+
+
+def cpu_baseline(model_cfg, computed_per_cand_step: float, n_branch: int):
+    """The float64 oracle on a bounded sample of the workload: one
+    transformer block at full token count with R1 and R2 sampled query rows
+    (keys/values of all tokens), extrapolated linearly to all rows, times
+    the block count, times the transformer calls per candidate-step the GPU
+    run measured."""
+    import dataclasses
+
+    import numpy as np
+
+    from oracle import dit
+    from paper_2607_23159_amd import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    m1 = dataclasses.replace(model_cfg, n_blocks=1)
+    W = {k: v.astype(np.float64) for k, v in synth.unflatten(m1, synth.make_weights(m1)).items()}
+    x = synth.make_noise(m1, 1)[0]
+    emb = dit.text_embedding(synth.make_context(m1, 1), W)
+    L = m1.tokens
+    times = {}
+    R1, R2 = 256, 2048
+    for nr in (R1, R2):
+        rows = np.linspace(0, L - 1, nr).astype(np.int64)
+        t0 = time.perf_counter()
+        dit.velocity(x, 0.5, emb, W, m1, last_block_rows=rows)
+        times[nr] = time.perf_counter() - t0
+    per_row = (times[R2] - times[R1]) / (R2 - R1)
+    fixed = times[R1] - R1 * per_row
+    block_s = fixed + per_row * L
+    eval_s = block_s * model_cfg.n_blocks
+    cand_step_s = eval_s * computed_per_cand_step
+    return {"value": 1.0 / cand_step_s, "unit": "candidate-steps/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"float64 oracle, one {model_cfg.hidden}-wide block at {L} tokens with {R1} and {R2} "
+                       f"sampled query rows ({times[R1]:.1f} s, {times[R2]:.1f} s), extrapolated to all "
+                       f"rows x {model_cfg.n_blocks} blocks = {eval_s:.0f} s per transformer call, "
+                       f"x {computed_per_cand_step:.3f} calls per candidate-step (measured on the GPU run, "
+                       f"B={n_branch})")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(candidates would shard across GPUs with no per-step traffic); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_23159_amd import binding as B
+    from paper_2607_23159_amd import synth
+    from paper_2607_23159_amd.search import GpuModel, Inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    B.lib()
+    dtype = synth.DTYPE_FP32 if args.fp32 else synth.DTYPE_BF16
+    nb = 2 if args.cfg else 1
+    t_gen = time.perf_counter()
+    wl = synth.make_workload(args.workload, n_branch=nb, dtype=dtype, n_cand=args.n_cand,
+                             n_steps=args.n_steps, tau=args.tau)
+    m, r = wl.model, wl.roll
+    gen_s = time.perf_counter() - t_gen
+    gm = GpuModel(m, wl.weights)
+    inp = Inputs(wl)
+    wl.weights = None
+    N, T = r.n_cand, r.n_steps
+    S = N * nb
+
+    def rollout(mode=None, timed_profile=False):
+        desc = B.RolloutDesc(r, wl.timesteps, **({} if mode is None else {"mode": mode}))
+        h = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[1] if nb == 2 else None)
+        try:
+            for k in range(1, T + 1):
+                B.cs_denoise_step(h, k)
+            scores = B.cs_score(h, inp.w, N)
+            st = B.cs_rollout_stats(h)
+            return scores, int(st.computed), int(st.calls)
+        finally:
+            B.cs_rollout_free(h)
+
+    # prime: load every kernel once (one transformer call), untimed
+    v = torch.empty_like(inp.x1[:1])
+    B.cs_velocity(gm.h, inp.x1[:1], 1, 1.0, inp.ctx[0], v)
+    torch.cuda.synchronize()
+
+    ref_scores = None
+    if args.reference:
+        ref_scores, _, _ = rollout(mode=synth.CACHE_OFF)
+
+    for _ in range(args.warmup):
+        rollout()
+    torch.cuda.synchronize()
+
+    if not args.no_profile:
+        B.cs_profile_enable(gm.h, True)
+        B.cs_profile_reset(gm.h)
+    computed = calls = 0
+    rho = top1 = None
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        scores, c, n = rollout()
+        computed += c
+        calls += n
+        if ref_scores is not None:
+            _, _, rho, top1 = B.cs_rank(scores, ref_scores)
+        else:
+            B.cs_rank(scores, scores)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    value = N * T * args.steps / wall
+
+    fam = {}
+    if not args.no_profile:
+        for f, name in enumerate(B.KERNEL_FAMILIES):
+            fam[name] = B.cs_profile_read(gm.h, f)
+        B.cs_profile_enable(gm.h, False)
+
+    L, d = m.tokens, m.hidden
+    evals = computed                                   # stream evaluations in the timed region
+    roof = None
+    if fam:
+        sa_ms, sa_n = fam["self_attn"]
+        flops = 4.0 * L * L * d * m.n_blocks * evals   # QK^T and PV, 2 flop per MAC
+        ach = flops / (sa_ms * 1e-3) / 1e12 if sa_ms > 0 else 0.0
+        peak = PEAK_FP32_TFLOPS if args.fp32 else PEAK_BF16_TFLOPS
+        roof = {"bound": "mfma", "kernel": "k_flash (self-attention)", "achieved": round(ach, 1),
+                "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4), "traffic": None,
+                "launches": sa_n, "avg_launch_ms": round(sa_ms / max(sa_n, 1), 3),
+                "flop_per_launch": flops / max(sa_n, 1)}
+        g_ms, g_n = fam["gemm"]
+        F = m.ffn
+        gflops = evals * (2.0 * L * m.n_blocks * (3 * d * d + 3 * d * d + 2 * d * F) + 4.0 * L * d * m.patch_dim)
+        roof["gemm_tflops"] = round(gflops / (g_ms * 1e-3) / 1e12, 1) if g_ms > 0 else None
+        roof["family_ms"] = {k: round(vv[0], 2) for k, vv in fam.items()}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        try:
+            cpu = cpu_baseline(m, computed / (N * T * args.steps), nb)
+        except Exception as e:  # report, never hide
+            cpu = {"value": None, "error": repr(e)}
+
+    out = {
+        "metric": "cached candidate denoise-steps/s (N seeds, 1 GPU)",
+        "value": round(value, 4),
+        "unit": "candidate-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if args.fp32 else "bf16",
+        "data": "synthetic",
+        "config": {"workload": (f"{args.workload}: Wan-shaped DiT {m.n_blocks} blocks d={d} "
+                                f"{m.heads}x{m.head_dim} ffn={m.ffn}, {L} tokens, N={N} seeds, "
+                                f"T={T}, tau={r.tau}, B={nb}, random init"),
+                   "n_cand": N, "n_steps": T, "tau": r.tau, "n_branch": nb,
+                   "cache_mode": r.mode},
+        "skip_fraction": round(1.0 - computed / max(calls, 1), 4),
+        "rho_vs_full": rho,
+        "top1_vs_full": top1,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "input_gen_s": round(gen_s, 1),
+    }
+    print(json.dumps(out), flush=True)
+    gm.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,7 +1,12 @@
 // Flash attention for gfx950: softmax(q k^T / sqrt(dh)) v per (stream, head),
 // non-causal, online softmax in fp32, MFMA for both products.
 //
-// Orientation.  Each wave owns QB blocks of 32 queries.  It computes the
+// Work split.  A workgroup of NW waves shares each K/V tile; each wave owns
+// QB blocks of 32 queries.  With 8 waves of one 32-query block, a wave needs
+// about 200 registers, so two waves fit per SIMD and the hardware overlaps
+// one wave's softmax (VALU) with the other's matrix products.
+//
+// Orientation.  Each wave computes the
 // transposed scores S^T = K Q^T (A = K tile from LDS, B = Q^T held in
 // registers for the whole key loop), so that after the softmax the
 // probabilities P^T already sit in the B-operand layout of the second
@@ -23,8 +28,10 @@
 
 namespace cs {
 
-template <typename T, int DH, int QB, int KVT>
-__global__ __launch_bounds__(256, 1) void k_flash(AttnArgs<T> a) {
+constexpr float RESCALE_LOG2 = 8.0f;
+
+template <typename T, int DH, int QB, int KVT, int NW>
+__global__ __launch_bounds__(64 * NW, NW / 4) void k_flash(AttnArgs<T> a) {
   typedef Mfma32<T> MF;
   constexpr int KPL = MF::KPL, KSTEP = MF::KSTEP;
   constexpr int CH = 16 / (int)sizeof(T);
@@ -34,9 +41,10 @@ __global__ __launch_bounds__(256, 1) void k_flash(AttnArgs<T> a) {
   constexpr int NDT = DH / 32;    // 32-channel blocks of the output
   constexpr int NKS = DH / KSTEP; // k-steps of the score product
   constexpr int NPS = 32 / KSTEP; // k-steps of the value product per key block
-  constexpr int K_CH = KVT * DH / CH / 256;
-  constexpr int V_CH = DH * KVT / CH / 256;
-  static_assert(K_CH * CH * 256 == KVT * DH && V_CH * CH * 256 == DH * KVT, "tile split");
+  constexpr int NT = 64 * NW;     // threads per workgroup
+  constexpr int K_CH = KVT * DH / CH / NT;
+  constexpr int V_CH = DH * KVT / CH / NT;
+  static_assert(K_CH * CH * NT == KVT * DH && V_CH * CH * NT == DH * KVT, "tile split");
   static_assert(CH % 4 == 0, "4-element groups");
 
   __shared__ __attribute__((aligned(16))) T sK[2][KVT * KLD];
@@ -46,7 +54,7 @@ __global__ __launch_bounds__(256, 1) void k_flash(AttnArgs<T> a) {
   const int half = lane >> 5, l32 = lane & 31;
   const int head = blockIdx.y, s = blockIdx.z;
   const int kvs = a.kv_sel ? a.kv_sel[s] : s;
-  const int q0 = blockIdx.x * (4 * QB * 32) + wave * QB * 32;
+  const int q0 = blockIdx.x * (NW * QB * 32) + wave * QB * 32;
 
   const T* qb_ = a.q + (long)s * a.q_ss + head * DH;
   const T* kb_ = a.k + (long)kvs * a.k_ss + head * DH;
@@ -67,14 +75,14 @@ __global__ __launch_bounds__(256, 1) void k_flash(AttnArgs<T> a) {
   auto load_tile = [&](int kv0) {
 #pragma unroll
     for (int c = 0; c < K_CH; ++c) {
-      const int id = c * 256 + tid;
+      const int id = c * NT + tid;
       const int r = id / (DH / CH), cc = id % (DH / CH);
       const int key = min(kv0 + r, a.lk - 1);
       rk[c] = ld16(kb_ + (long)key * a.k_ld + cc * CH);
     }
 #pragma unroll
     for (int c = 0; c < V_CH; ++c) {
-      const int id = c * 256 + tid;
+      const int id = c * NT + tid;
       const int r = id / (KVT / CH), cc = id % (KVT / CH);
       rv[c] = ld16(vb_ + (long)r * a.vt_ld + kv0 + cc * CH);
     }
@@ -82,13 +90,13 @@ __global__ __launch_bounds__(256, 1) void k_flash(AttnArgs<T> a) {
   auto store_tile = [&](int buf) {
 #pragma unroll
     for (int c = 0; c < K_CH; ++c) {
-      const int id = c * 256 + tid;
+      const int id = c * NT + tid;
       const int r = id / (DH / CH), cc = id % (DH / CH);
       st16(&sK[buf][r * KLD + cc * CH], rk[c]);
     }
 #pragma unroll
     for (int c = 0; c < V_CH; ++c) {
-      const int id = c * 256 + tid;
+      const int id = c * NT + tid;
       const int r = id / (KVT / CH), cc = id % (KVT / CH);
       // groups of 4 consecutive keys stay contiguous under the permutation
       const T* src = reinterpret_cast<const T*>(&rv[c]);
@@ -159,7 +167,12 @@ __global__ __launch_bounds__(256, 1) void k_flash(AttnArgs<T> a) {
         }
     }
 
-    // online softmax; P^T packed into B-operand fragments
+    // online softmax; P^T packed into B-operand fragments.  The running
+    // maximum is only raised (and O, l rescaled) when some lane's tile
+    // maximum exceeds it by more than RESCALE_LOG2; otherwise the stale
+    // maximum is kept and probabilities may reach 2^RESCALE_LOG2, which fp32
+    // accumulation and the bf16 operand carry without loss of relative
+    // precision.  The branch is uniform across the wave.
     typename MF::frag pf[QB][NKT][NPS];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -168,22 +181,25 @@ __global__ __launch_bounds__(256, 1) void k_flash(AttnArgs<T> a) {
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][qb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
-      const float m_new = fmaxf(m_run[qb], mx * a.scale_log2);
-      const float alpha = exp2f(m_run[qb] - m_new);
-      m_run[qb] = m_new;
-      l_run[qb] *= alpha;
+      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * a.scale_log2;
+      if (__any(mx > m_run[qb] + RESCALE_LOG2)) {
+        const float m_new = fmaxf(m_run[qb], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
+        for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[qb][dt][r] *= alpha;
+          for (int r = 0; r < 16; ++r) o[qb][dt][r] *= alpha;
+      }
+      const float m_cur = m_run[qb];
       float lsum = 0.0f;
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt) {
         float p[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          p[r] = exp2f(fmaf(sc[kt][qb][r], a.scale_log2, -m_new));
+          p[r] = __builtin_amdgcn_exp2f(fmaf(sc[kt][qb][r], a.scale_log2, -m_cur));
           lsum += p[r];
         }
 #pragma unroll
@@ -242,11 +258,11 @@ int attn_kv_tile(int dtype_bytes, int head_dim) {
   return (dtype_bytes == 4 && head_dim > 64) ? 32 : 64;
 }
 
-template <typename T, int DH, int QB, int KVT>
+template <typename T, int DH, int QB, int KVT, int NW>
 static hipError_t launch_flash(const AttnArgs<T>& a, hipStream_t st) {
-  const int qpw = 4 * QB * 32;
+  const int qpw = NW * QB * 32;
   dim3 grid((unsigned)cdiv(a.lq, qpw), (unsigned)a.heads, (unsigned)a.n_streams);
-  hipLaunchKernelGGL((k_flash<T, DH, QB, KVT>), grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL((k_flash<T, DH, QB, KVT, NW>), grid, dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 
@@ -254,9 +270,9 @@ template <>
 hipError_t flash_attention<bf16>(const AttnArgs<bf16>& a, int head_dim, hipStream_t st) {
   if (a.lq <= 0 || a.n_streams <= 0) return hipSuccess;
   switch (head_dim) {
-    case 128: return launch_flash<bf16, 128, 2, 64>(a, st);
-    case 64: return launch_flash<bf16, 64, 2, 64>(a, st);
-    case 32: return launch_flash<bf16, 32, 2, 64>(a, st);
+    case 128: return launch_flash<bf16, 128, 1, 64, 8>(a, st);
+    case 64: return launch_flash<bf16, 64, 1, 64, 8>(a, st);
+    case 32: return launch_flash<bf16, 32, 1, 64, 4>(a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -265,9 +281,9 @@ template <>
 hipError_t flash_attention<float>(const AttnArgs<float>& a, int head_dim, hipStream_t st) {
   if (a.lq <= 0 || a.n_streams <= 0) return hipSuccess;
   switch (head_dim) {
-    case 128: return launch_flash<float, 128, 1, 32>(a, st);
-    case 64: return launch_flash<float, 64, 1, 64>(a, st);
-    case 32: return launch_flash<float, 32, 1, 64>(a, st);
+    case 128: return launch_flash<float, 128, 1, 32, 4>(a, st);
+    case 64: return launch_flash<float, 64, 1, 64, 4>(a, st);
+    case 32: return launch_flash<float, 32, 1, 64, 4>(a, st);
     default: return hipErrorInvalidValue;
   }
 }
