@@ -60,10 +60,14 @@ struct alignas(16) Chunk16 { uint32_t w[4]; };
 CS_DEV Chunk16 ld16(const void* p) { return *reinterpret_cast<const Chunk16*>(p); }
 CS_DEV void st16(void* p, Chunk16 c) { *reinterpret_cast<Chunk16*>(p) = c; }
 
+// GELU, tanh form, with tanh(u) = 1 - 2 / (1 + 2^(2 u log2 e)) on the
+// hardware exp2 and reciprocal (saturates correctly to +-1 for large |u|).
 CS_DEV float gelu_tanh(float x) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  float u = k0 * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.0f + tanhf(u));
+  const float u = k0 * (x + 0.044715f * x * x * x);
+  const float e = __builtin_amdgcn_exp2f(u * 2.8853900817779268f);  // e^(2u)
+  const float t = 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + e);
+  return 0.5f * x * (1.0f + t);
 }
 CS_DEV float silu(float x) { return x / (1.0f + expf(-x)); }
 
