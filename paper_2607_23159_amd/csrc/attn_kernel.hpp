@@ -1,0 +1,267 @@
+// Flash attention for gfx950: softmax(q k^T / sqrt(dh)) v per (stream, head),
+// non-causal, online softmax in fp32, MFMA for both products.
+//
+// Work split.  A workgroup of NW waves shares each K/V tile; each wave owns
+// QB blocks of 32 queries.  With 8 waves of one 32-query block, a wave needs
+// about 200 registers, so two waves fit per SIMD and the hardware overlaps
+// one wave's softmax (VALU) with the other's matrix products.
+//
+// Orientation.  Each wave computes the
+// transposed scores S^T = K Q^T (A = K tile from LDS, B = Q^T held in
+// registers for the whole key loop), so that after the softmax the
+// probabilities P^T already sit in the B-operand layout of the second
+// product O^T = V^T P^T (A = V^T tile from LDS).  The MFMA's contraction
+// index may visit keys in any order as long as both operands agree: the
+// accumulator register j of lane l holds key 8(j/4) + 4(l/32) + j%4 of a
+// 32-key block, so the V^T tile is written to LDS with each 32-key block
+// permuted to position 16(l/32) + j.  No shuffle of P through LDS is needed.
+//
+// The softmax row of query q lives in lanes l and l^32 (16 keys each per
+// 32-key block), so row maxima and sums need one cross-lane exchange.
+//
+// K and V^T tiles of KVT keys are staged through LDS, double buffered (the
+// next tile's global loads are in flight during the current tile's math).
+// Keys past lk are masked to -inf in the last tile; K rows past lk are read
+// clamped and V^T columns past lk must be finite (the runtime zero-fills the
+// padding of every V^T buffer).
+#pragma once
+#include "kernels.hpp"
+
+namespace cs {
+
+constexpr float RESCALE_LOG2 = 8.0f;
+
+// OCC is the number of waves per SIMD the register budget is sized for.
+// CROSS distinguishes the cross-attention instantiation (text keys) from the
+// self-attention one, so that profiles report them separately.
+template <typename T, int DH, int QB, int KVT, int NW, int OCC, bool CROSS>
+__global__ __launch_bounds__(64 * NW, OCC) void k_flash(AttnArgs<T> a) {
+  typedef Mfma32<T> MF;
+  constexpr int KPL = MF::KPL, KSTEP = MF::KSTEP;
+  constexpr int CH = 16 / (int)sizeof(T);
+  constexpr int KLD = DH + CH;    // padded K row (16 bytes)
+  constexpr int VLD = KVT + CH;   // padded V^T row
+  constexpr int NKT = KVT / 32;   // 32-key blocks per tile
+  constexpr int NDT = DH / 32;    // 32-channel blocks of the output
+  constexpr int NKS = DH / KSTEP; // k-steps of the score product
+  constexpr int NPS = 32 / KSTEP; // k-steps of the value product per key block
+  constexpr int NT = 64 * NW;     // threads per workgroup
+  constexpr int K_CH = KVT * DH / CH / NT;
+  constexpr int V_CH = DH * KVT / CH / NT;
+  static_assert(K_CH * CH * NT == KVT * DH && V_CH * CH * NT == DH * KVT, "tile split");
+  static_assert(CH % 4 == 0, "4-element groups");
+
+  __shared__ __attribute__((aligned(16))) T sK[2][KVT * KLD];
+  __shared__ __attribute__((aligned(16))) T sV[2][DH * VLD];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int head = blockIdx.y, s = blockIdx.z;
+  const int kvs = a.kv_sel ? a.kv_sel[s] : s;
+  const int q0 = blockIdx.x * (NW * QB * 32) + wave * QB * 32;
+
+  const T* qb_ = a.q + (long)s * a.q_ss + head * DH;
+  const T* kb_ = a.k + (long)kvs * a.k_ss + head * DH;
+  const T* vb_ = a.vt + (long)kvs * a.vt_ss + (long)head * DH * a.vt_ld;
+
+  // Q^T fragments (B operand), kept for the whole key loop.
+  typename MF::frag qf[QB][NKS];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int row = min(q0 + qb * 32 + l32, a.lq - 1);
+    const T* src = qb_ + (long)row * a.q_ld + KPL * half;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[qb][ks] = MF::load(src + ks * KSTEP);
+  }
+
+  // tile staging
+  Chunk16 rk[K_CH], rv[V_CH];
+  auto load_tile = [&](int kv0) {
+#pragma unroll
+    for (int c = 0; c < K_CH; ++c) {
+      const int id = c * NT + tid;
+      const int r = id / (DH / CH), cc = id % (DH / CH);
+      const int key = min(kv0 + r, a.lk - 1);
+      rk[c] = ld16(kb_ + (long)key * a.k_ld + cc * CH);
+    }
+#pragma unroll
+    for (int c = 0; c < V_CH; ++c) {
+      const int id = c * NT + tid;
+      const int r = id / (KVT / CH), cc = id % (KVT / CH);
+      rv[c] = ld16(vb_ + (long)r * a.vt_ld + kv0 + cc * CH);
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < K_CH; ++c) {
+      const int id = c * NT + tid;
+      const int r = id / (DH / CH), cc = id % (DH / CH);
+      st16(&sK[buf][r * KLD + cc * CH], rk[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < V_CH; ++c) {
+      const int id = c * NT + tid;
+      const int r = id / (KVT / CH), cc = id % (KVT / CH);
+      // groups of 4 consecutive keys stay contiguous under the permutation
+      const T* src = reinterpret_cast<const T*>(&rv[c]);
+#pragma unroll
+      for (int g = 0; g < CH / 4; ++g) {
+        const int key = cc * CH + 4 * g;            // key inside the tile
+        const int w = key & 31;
+        const int pos = (key & ~31) + 16 * ((w >> 2) & 1) + 4 * (w >> 3);
+        T* dst = &sV[buf][r * VLD + pos];
+        if (sizeof(T) == 2) {
+          *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(src + 4 * g);
+        } else {
+          *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src + 4 * g);
+        }
+      }
+    }
+  };
+
+  f32x16 o[QB][NDT];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[qb][dt][r] = 0.0f;
+  float m_run[QB], l_run[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.0f; }
+
+  const int ntiles = (a.lk + KVT - 1) / KVT;
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int cur = t & 1;
+    const int kv0 = t * KVT;
+    const bool more = t + 1 < ntiles;
+    if (more) load_tile(kv0 + KVT);
+
+    // S^T = K Q^T
+    f32x16 sc[NKT][QB];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[kt][qb][r] = 0.0f;
+    const T* pk = &sK[cur][l32 * KLD + KPL * half];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        typename MF::frag kf = MF::load(pk + kt * 32 * KLD + ks * KSTEP);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) sc[kt][qb] = MF::mma(kf, qf[qb][ks], sc[kt][qb]);
+      }
+    }
+    if (kv0 + KVT > a.lk) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kv0 + kt * 32 + acc_row(r, lane);
+          if (key >= a.lk)
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) sc[kt][qb][r] = -INFINITY;
+        }
+    }
+
+    // online softmax; P^T packed into B-operand fragments.  The running
+    // maximum is only raised (and O, l rescaled) when some lane's tile
+    // maximum exceeds it by more than RESCALE_LOG2; otherwise the stale
+    // maximum is kept and probabilities may reach 2^RESCALE_LOG2, which fp32
+    // accumulation and the bf16 operand carry without loss of relative
+    // precision.  The branch is uniform across the wave.
+    typename MF::frag pf[QB][NKT][NPS];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][qb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * a.scale_log2;
+      if (__any(mx > m_run[qb] + RESCALE_LOG2)) {
+        const float m_new = fmaxf(m_run[qb], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[qb][dt][r] *= alpha;
+      }
+      const float m_cur = m_run[qb];
+      float lsum = 0.0f;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        float p[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(sc[kt][qb][r], a.scale_log2, -m_cur));
+#pragma unroll
+        for (int ps = 0; ps < NPS; ++ps) {
+          if constexpr (KPL == 1) {
+            pf[qb][kt][ps] = to_t<T>(p[ps]);
+            lsum += p[ps];
+          } else {
+            // the row sum is taken over the rounded operand that the value
+            // product consumes, two elements per dot instruction
+            typename MF::frag f;
+#pragma unroll
+            for (int i = 0; i < KPL; ++i) f[i] = to_t<T>(p[ps * KPL + i]);
+            pf[qb][kt][ps] = f;
+            const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+#pragma unroll
+            for (int i = 0; i < KPL; i += 2) {
+              const bf16x2 pr = {f[i], f[i + 1]};
+              lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, one, lsum, false);
+            }
+          }
+        }
+      }
+      l_run[qb] += lsum;
+    }
+
+    // O^T += V^T P^T
+    const T* pv = &sV[cur][l32 * VLD + 16 * half];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int ps = 0; ps < NPS; ++ps)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          typename MF::frag vf = MF::load(pv + dt * 32 * VLD + kt * 32 + ps * KPL);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) o[qb][dt] = MF::mma(vf, pf[qb][kt][ps], o[qb][dt]);
+        }
+
+    if (more) store_tile(cur ^ 1);
+    __syncthreads();
+  }
+
+  // normalise and store O[q][head*DH + channel]
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32, WAVE);
+    const float inv = 1.0f / l_tot;
+    const int row = q0 + qb * 32 + l32;
+    if (row < a.lq) {
+      T* dst = a.o + (long)s * a.o_ss + (long)row * a.o_ld + head * DH;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int ch = dt * 32 + 8 * g + 4 * half;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) dst[ch + r] = to_t<T>(o[qb][dt][4 * g + r] * inv);
+        }
+    }
+  }
+}
+
+}  // namespace cs

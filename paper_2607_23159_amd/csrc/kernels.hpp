@@ -31,7 +31,7 @@ template <typename T> struct AttnArgs {
   const T* q; long q_ld; long q_ss;     // stream s: rows at q + s*q_ss, row stride q_ld
   const T* k; long k_ld; long k_ss;     // keys of kv stream j at k + j*k_ss
   const T* vt; long vt_ld; long vt_ss;  // values transposed: row = channel, col = key
-  const int* kv_sel;                    // stream -> kv stream (NULL: identity)
+  const int* kv_sel;                    // stream -> kv stream (NULL: identity, self-attention)
   T* o; long o_ld; long o_ss;
   int lq, lk, heads, n_streams;
   float scale_log2;                     // log2(e) / sqrt(head_dim)
