@@ -64,8 +64,8 @@ typedef enum { CS_CACHE_OFF = 0, CS_CACHE_ADAPTIVE = 1, CS_CACHE_STATIC = 2 } cs
  * RMSNorm q/k and 3D RoPE, cross-attention to the text embedding,
  * adaLN tanh-GELU FFN], adaLN head.  Requirements: hidden = heads*head_dim,
  * head_dim in {32, 64, 128}, hidden % 64 == 0, ffn % 64 == 0,
- * text_dim % 64 == 0, freq_dim == 256, patch = (1,2,2), lat_h and lat_w
- * even.  dtype selects the transformer's matrix arithmetic (bf16 operands
+ * text_dim % 64 == 0, in_ch % 16 == 0, freq_dim == 256, patch = (1,2,2),
+ * lat_h and lat_w even.  dtype selects the transformer's matrix arithmetic (bf16 operands
  * with fp32 accumulation, or fp32 throughout); the cache state, latents,
  * residual stream and all reductions are fp32/fp64 in both modes. */
 typedef struct {

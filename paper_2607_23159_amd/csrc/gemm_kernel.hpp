@@ -35,8 +35,9 @@ struct GemmShape {
   static_assert(A_CH * NT == BM * CPR && B_CH * NT == BN * CPR, "slice split");
 };
 
-// OCC = waves per SIMD the register budget is sized for.
-template <typename T, int BM, int BN, int BK, int WM, int WN, int NWAVE, int OCC, class Epi>
+// OCC = waves per SIMD the register budget is sized for; GM = tile-rows per
+// group of the tile order (1 = row-major).
+template <typename T, int BM, int BN, int BK, int WM, int WN, int NWAVE, int OCC, int GM, class Epi>
 __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ A, long lda,
                                                         const T* __restrict__ W, long ldw, int M,
                                                         int N, int K, Epi epi) {
@@ -52,14 +53,29 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
   const int wm = wave / S::WAVES_N, wn = wave % S::WAVES_N;
 
   // Tile order: the launch is split into 8 contiguous ranges, one per XCD
-  // (workgroups are dealt round-robin to the 8 dies), so tiles that share
-  // rows of A run on the same die and share its L2.
+  // (workgroups are dealt round-robin to the 8 dies).  Inside a range, tiles
+  // are visited in groups of GM tile-rows, column-major within the group, so
+  // the workgroups resident on one die at a time share both rows of A and
+  // columns of W in its L2.
   const int tiles_n = (N + BN - 1) / BN;
+  const int tiles_m = (M + BM - 1) / BM;
   const int nwg = gridDim.x;
   int bid = blockIdx.x;
   if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
-  const int m0 = (bid / tiles_n) * BM;
-  const int n0 = (bid % tiles_n) * BN;
+  int tm_i, tn_i;
+  if (GM > 1) {
+    const int group = bid / (GM * tiles_n);
+    const int first_m = group * GM;
+    const int gm = min(tiles_m - first_m, GM);
+    const int in = bid - group * GM * tiles_n;
+    tm_i = first_m + in % gm;
+    tn_i = in / gm;
+  } else {
+    tm_i = bid / tiles_n;
+    tn_i = bid % tiles_n;
+  }
+  const int m0 = tm_i * BM;
+  const int n0 = tn_i * BN;
 
   // global -> register staging
   Chunk16 ra[S::A_CH], rb[S::B_CH];
@@ -136,7 +152,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
 #pragma unroll
       for (int i = 0; i < S::TM; ++i)
 #pragma unroll
-        for (int j = 0; j < S::TN; ++j) acc[i][j] = MF::mma(fa[c][i], fb[c][j], acc[i][j]);
+        for (int j = 0; j < S::TN; ++j) acc[i][j] = MF::mma(fb[c][j], fa[c][i], acc[i][j]);
     }
     if (more) {
       const int nxt = cur ^ 1;
@@ -148,37 +164,223 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
     __syncthreads();
   }
 
-  // epilogue: each lane owns, per accumulator, 4 groups of 4 consecutive rows
-  // of one column.
+  // epilogue: the products were formed as C^T tiles (W fragment as the MFMA A
+  // operand), so each lane owns, per accumulator, one row and 4 groups of 4
+  // consecutive columns; every group becomes one vector access.
 #pragma unroll
-  for (int i = 0; i < S::TM; ++i)
+  for (int i = 0; i < S::TM; ++i) {
+    const int row = m0 + wm * WM + i * 32 + (lane & 31);
+    if (row >= M) continue;
 #pragma unroll
-    for (int j = 0; j < S::TN; ++j) {
-      const int col = n0 + wn * WN + j * 32 + (lane & 31);
-      if (col >= N) continue;
+    for (int j = 0; j < S::TN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int row0 = m0 + wm * WM + i * 32 + 8 * g + 4 * (lane >> 5);
-        float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                      acc[i][j][4 * g + 3]};
-        epi(row0, col, v, M);
+        const int col0 = n0 + wn * WN + j * 32 + 8 * g + 4 * (lane >> 5);
+        if (col0 >= N) continue;
+        const float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                            acc[i][j][4 * g + 3]};
+        epi(row, col0, v);
       }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 GEMM with direct global->LDS loads (gfx950 global_load_lds_dwordx4).
+//
+// Each load instruction of a wave moves 64 x 16 bytes into 1 KB of LDS at
+// base + 16*lane, with an arbitrary global address per lane, so no registers
+// stage the tiles and no LDS store instructions are issued.  K slices rotate
+// through a ring of STAGES buffers: slice k+STAGES-1 is requested while slice
+// k is multiplied, and a wave waits (vmcnt) only for slice k before the single
+// barrier of each iteration.  LDS rows are unpadded; the 16-byte chunk c of
+// row r is stored at chunk c ^ f(r), f(r) = (r ^ (r >> log2 CPR)) & (CPR-1),
+// which keeps the 32-row fragment reads free of bank conflicts.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
+
+template <int CPR> CS_DEV int chunk_swz(int r) {
+  constexpr int LOG = CPR == 4 ? 2 : (CPR == 8 ? 3 : 1);
+  return (r ^ (r >> LOG)) & (CPR - 1);
+}
+
+// Wait until at most n vector-memory operations of this wave are
+// outstanding, then barrier; the memory clobber keeps the compiler from moving
+// LDS accesses across it.
+template <int n> CS_DEV void wait_vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(n) : "memory");
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int NWAVE, int OCC, int STAGES, int GM,
+          class Epi>
+__global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restrict__ A, long lda,
+                                                           const bf16* __restrict__ W, long ldw,
+                                                           int M, int N, int K, Epi epi) {
+  typedef Mfma32<bf16> MF;
+  constexpr int CH = 8;                       // bf16 per 16-byte chunk
+  constexpr int CPR = BK / CH;                // chunks per LDS row
+  constexpr int RPI = 64 / CPR;               // rows filled by one wave instruction
+  constexpr int A_INST = BM / RPI / NWAVE;    // load instructions per wave per slice
+  constexpr int B_INST = BN / RPI / NWAVE;
+  constexpr int PER_SLICE = A_INST + B_INST;
+  constexpr int STAGE = (BM + BN) * BK;       // elements per stage
+  constexpr int WAVES_N = BN / WN;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int KS = BK / MF::KSTEP;
+  static_assert(A_INST * RPI * NWAVE == BM && B_INST * RPI * NWAVE == BN, "load split");
+  static_assert((BM / WM) * WAVES_N == NWAVE, "wave grid");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[STAGES * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+  const int tiles_n = (N + BN - 1) / BN;
+  const int tiles_m = (M + BM - 1) / BM;
+  const int nwg = gridDim.x;
+  int bid = blockIdx.x;
+  if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  int tm_i, tn_i;
+  if (GM > 1) {
+    const int group = bid / (GM * tiles_n);
+    const int first_m = group * GM;
+    const int gm = min(tiles_m - first_m, GM);
+    const int in = bid - group * GM * tiles_n;
+    tm_i = first_m + in % gm;
+    tn_i = in / gm;
+  } else {
+    tm_i = bid / tiles_n;
+    tn_i = bid % tiles_n;
+  }
+  const int m0 = tm_i * BM, n0 = tn_i * BN;
+
+  // per-lane sources: lane covers row (lane / CPR) of its instruction's rows
+  // and physical chunk lane % CPR, i.e. logical chunk phys ^ f(row)
+  const bf16* a_src[A_INST];
+  const bf16* b_src[B_INST];
+  {
+    const int rin = lane / CPR, phys = lane % CPR;
+#pragma unroll
+    for (int i = 0; i < A_INST; ++i) {
+      const int row = (wave * A_INST + i) * RPI + rin;
+      const int gr = min(m0 + row, M - 1);
+      a_src[i] = A + (long)gr * lda + (phys ^ chunk_swz<CPR>(row)) * CH;
     }
+#pragma unroll
+    for (int i = 0; i < B_INST; ++i) {
+      const int row = (wave * B_INST + i) * RPI + rin;
+      const int gr = min(n0 + row, N - 1);
+      b_src[i] = W + (long)gr * ldw + (phys ^ chunk_swz<CPR>(row)) * CH;
+    }
+  }
+  auto issue = [&](int slice, int st) {
+    const long koff = (long)slice * BK;
+    bf16* sa = smem + st * STAGE;
+    bf16* sb = sa + BM * BK;
+#pragma unroll
+    for (int i = 0; i < A_INST; ++i)
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(a_src[i] + koff),
+                                       (lds_void_t*)(sa + (wave * A_INST + i) * RPI * BK), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < B_INST; ++i)
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(b_src[i] + koff),
+                                       (lds_void_t*)(sb + (wave * B_INST + i) * RPI * BK), 16, 0, 0);
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = K / BK;
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  // fragment addressing: lane reads row (lane & 31) of each 32-row block at
+  // logical chunk 2*ks + (lane >> 5)
+  const int a_row0 = wm * WM + (lane & 31);
+  const int b_row0 = wn * WN + (lane & 31);
+  const int half = lane >> 5;
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int rem = nk - 1 - kt;  // slices requested after slice kt
+    if (rem >= STAGES - 2) wait_vm_barrier<(STAGES - 2) * PER_SLICE>();
+    else if (STAGES > 3 && rem == 1) wait_vm_barrier<(STAGES > 3 ? 1 : 0) * PER_SLICE>();
+    else wait_vm_barrier<0>();
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    const bf16* sa = smem + (kt % STAGES) * STAGE;
+    const bf16* sb = sa + BM * BK;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int c = 2 * ks + half;
+      typename MF::frag fa[TM], fb[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r = a_row0 + i * 32;
+        fa[i] = MF::load(sa + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int r = b_row0 + j * 32;
+        fb[j] = MF::load(sb + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = MF::mma(fb[j], fa[i], acc[i][j]);
+    }
+  }
+
+  // epilogue: the products were formed as C^T tiles (W fragment as the MFMA A
+  // operand), so each lane owns, per accumulator, one row and 4 groups of 4
+  // consecutive columns; every group becomes one vector access.
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int row = m0 + wm * WM + i * 32 + (lane & 31);
+    if (row >= M) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int col0 = n0 + wn * WN + j * 32 + 8 * g + 4 * (lane >> 5);
+        if (col0 >= N) continue;
+        const float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                            acc[i][j][4 * g + 3]};
+        epi(row, col0, v);
+      }
+  }
 }
 
 // ------------------------------------------------------------- epilogues
+// Called per (row, 4 consecutive columns col0..col0+3); N is a multiple of 4.
+template <typename T> CS_DEV void store4(T* p, const float* y) {
+  if constexpr (sizeof(T) == 2) {
+    bf16x4 q;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) q[r] = to_t<T>(y[r]);
+    *reinterpret_cast<bf16x4*>(p) = q;
+  } else {
+    *reinterpret_cast<float4*>(p) = make_float4(y[0], y[1], y[2], y[3]);
+  }
+}
+CS_DEV float4 load_bias4(const float* b, int col0) {
+  return b ? *reinterpret_cast<const float4*>(b + col0) : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
 template <typename T> struct EpiStore {
   T* out; long ldo; const float* bias; int act;  // act: 0 none, 1 tanh-GELU
-  CS_DEV void operator()(int row0, int col, const float* v, int M) const {
-    const float b = bias ? bias[col] : 0.0f;
+  CS_DEV void operator()(int row, int col0, const float* v) const {
+    const float4 b = load_bias4(bias, col0);
+    float y[4] = {v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w};
+    if (act == 1) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      if (row0 + r < M) {
-        float y = v[r] + b;
-        if (act == 1) y = gelu_tanh(y);
-        out[(long)(row0 + r) * ldo + col] = to_t<T>(y);
-      }
+      for (int r = 0; r < 4; ++r) y[r] = gelu_tanh(y[r]);
     }
+    store4<T>(out + (long)row * ldo + col0, y);
   }
 };
 
@@ -187,37 +389,16 @@ template <typename T> struct EpiStore {
 // vT[stream][channel][token] with a padded token stride.
 template <typename T> struct EpiQKV {
   T* qk; T* vt; const float* bias; int d; int L; long vt_ld; long vt_ss;
-  CS_DEV void operator()(int row0, int col, const float* v, int M) const {
-    const float b = bias[col];
-    if (col < 2 * d) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (row0 + r < M) qk[(long)(row0 + r) * (2 * d) + col] = to_t<T>(v[r] + b);
+  CS_DEV void operator()(int row, int col0, const float* v) const {
+    const float4 b = load_bias4(bias, col0);
+    const float y[4] = {v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w};
+    if (col0 < 2 * d) {
+      store4<T>(qk + (long)row * (2 * d) + col0, y);
     } else {
-      const int c = col - 2 * d;
-      if ((L & 3) == 0 && row0 + 3 < M) {
-        // four consecutive tokens of one stream: one 8-byte store
-        const int s = row0 / L, tok = row0 - s * L;
-        T* dst = vt + (long)s * vt_ss + (long)c * vt_ld + tok;
-        if constexpr (sizeof(T) == 2) {
-          bf16x4 q;
+      const int s = row / L, tok = row - s * L;
+      T* dst = vt + (long)s * vt_ss + (long)(col0 - 2 * d) * vt_ld + tok;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) q[r] = to_t<T>(v[r] + b);
-          *reinterpret_cast<bf16x4*>(dst) = q;
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) dst[r] = v[r] + b;
-        }
-        return;
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = row0 + r;
-        if (row < M) {
-          const int s = row / L, tok = row - s * L;
-          vt[(long)s * vt_ss + (long)c * vt_ld + tok] = to_t<T>(v[r] + b);
-        }
-      }
+      for (int r = 0; r < 4; ++r) dst[(long)r * vt_ld] = to_t<T>(y[r]);
     }
   }
 };
@@ -225,59 +406,55 @@ template <typename T> struct EpiQKV {
 // Transposed store of a single-stream projection: out[col][row].
 template <typename T> struct EpiStoreT {
   T* out; long ldo; const float* bias;
-  CS_DEV void operator()(int row0, int col, const float* v, int M) const {
-    const float b = bias[col];
+  CS_DEV void operator()(int row, int col0, const float* v) const {
+    const float4 b = load_bias4(bias, col0);
+    const float y[4] = {v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w};
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (row0 + r < M) out[(long)col * ldo + row0 + r] = to_t<T>(v[r] + b);
+    for (int r = 0; r < 4; ++r) out[(long)(col0 + r) * ldo + row] = to_t<T>(y[r]);
   }
 };
 
 // Residual update z += gate * (acc + bias) (gate NULL: 1).
 struct EpiResidual {
   float* z; long ldz; const float* bias; const float* gate;
-  CS_DEV void operator()(int row0, int col, const float* v, int M) const {
-    const float b = bias[col];
-    const float g = gate ? gate[col] : 1.0f;
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (row0 + r < M) {
-        float* p = z + (long)(row0 + r) * ldz + col;
-        *p = *p + g * (v[r] + b);
-      }
+  CS_DEV void operator()(int row, int col0, const float* v) const {
+    const float4 b = load_bias4(bias, col0);
+    const float4 g = gate ? *reinterpret_cast<const float4*>(gate + col0) : make_float4(1.f, 1.f, 1.f, 1.f);
+    float4* p = reinterpret_cast<float4*>(z + (long)row * ldz + col0);
+    float4 o = *p;
+    o.x += g.x * (v[0] + b.x);
+    o.y += g.y * (v[1] + b.y);
+    o.z += g.z * (v[2] + b.z);
+    o.w += g.w * (v[3] + b.w);
+    *p = o;
   }
 };
 
 // Patch embedding: z = acc + bias (fp32 residual stream).
 struct EpiPatch {
   float* z; long ldz; const float* bias;
-  CS_DEV void operator()(int row0, int col, const float* v, int M) const {
-    const float b = bias[col];
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (row0 + r < M) z[(long)(row0 + r) * ldz + col] = v[r] + b;
+  CS_DEV void operator()(int row, int col0, const float* v) const {
+    const float4 b = load_bias4(bias, col0);
+    *reinterpret_cast<float4*>(z + (long)row * ldz + col0) =
+        make_float4(v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w);
   }
 };
 
 // Head: acc + bias, scattered back to latent layout (unpatchify).  Row
 // = slot * L + token (token = (f, h, w) row-major on the patch grid);
-// column = c*4 + dy*2 + dx.  The slot's output latent is out + slot_id[slot]*D.
+// columns c*4 .. c*4+3 are the 2x2 patch (dy, dx) of channel c.  The slot's
+// output latent is out + slot_id[slot] * D.
 struct EpiHead {
   float* out; const int* slot_id; const float* bias; int L, gh, gw, F, H, Wd; long D;
-  CS_DEV void operator()(int row0, int col, const float* v, int M) const {
-    const float b = bias[col];
-    const int c = col >> 2, dy = (col >> 1) & 1, dx = col & 1;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = row0 + r;
-      if (row < M) {
-        const int s = row / L, tok = row - s * L;
-        const int f = tok / (gh * gw), rem = tok - f * gh * gw;
-        const int hh = rem / gw, ww = rem - hh * gw;
-        float* dst = out + (long)slot_id[s] * D;
-        dst[(((long)c * F + f) * H + 2 * hh + dy) * Wd + 2 * ww + dx] = v[r] + b;
-      }
-    }
+  CS_DEV void operator()(int row, int col0, const float* v) const {
+    const float4 b = load_bias4(bias, col0);
+    const int c = col0 >> 2;
+    const int s = row / L, tok = row - s * L;
+    const int f = tok / (gh * gw), rem = tok - f * gh * gw;
+    const int hh = rem / gw, ww = rem - hh * gw;
+    float* dst = out + (long)slot_id[s] * D + (((long)c * F + f) * H + 2 * hh) * Wd + 2 * ww;
+    *reinterpret_cast<float2*>(dst) = make_float2(v[0] + b.x, v[1] + b.y);
+    *reinterpret_cast<float2*>(dst + Wd) = make_float2(v[2] + b.z, v[3] + b.w);
   }
 };
 

@@ -4,70 +4,88 @@
 namespace cs {
 
 // ------------------------------------------------------------- launchers
-// bf16: 256x256 tiles, 8 waves of 128x64 (two waves per SIMD), K slices of
-//       64 (147 KB of LDS, one workgroup per CU); the fastest of the shapes
-//       swept at the Wan2.1-1.3B projection sizes.
-// fp32: 128x128 tiles, 4 waves of 64x64, K slices of 16.
+// bf16: direct-to-LDS kernel, 256x256 tiles, 8 waves of 128x64 (two per
+//       SIMD), K slices of 64 in two LDS stages (128 KB), tile groups of 4
+//       tile-rows; the fastest shape of those swept at the Wan2.1-1.3B
+//       projection sizes.  K must be a multiple of 64.
+// fp32: register-staged kernel, 128x128 tiles, 4 waves of 64x64, K slices of 16.
+// Narrow N (head GEMM, N = patch_dim): register-staged 128x64 tiles.
 template <typename T> struct GemmCfg;
-template <> struct GemmCfg<bf16> {
-  static constexpr int BM = 256, BN = 256, BK = 64, WM = 128, WN = 64, NW = 8, OCC = 2;
-};
 template <> struct GemmCfg<float> {
-  static constexpr int BM = 128, BN = 128, BK = 16, WM = 64, WN = 64, NW = 4, OCC = 1;
+  static constexpr int BM = 128, BN = 128, BK = 16, WM = 64, WN = 64, NW = 4, OCC = 1, GM = 1;
 };
-// Narrow-N variant (head GEMM, N = patch_dim).
 template <typename T> struct GemmCfgNarrow;
 template <> struct GemmCfgNarrow<bf16> {
-  static constexpr int BM = 128, BN = 64, BK = 32, WM = 32, WN = 64, NW = 4, OCC = 1;
+  static constexpr int BM = 128, BN = 64, BK = 32, WM = 32, WN = 64, NW = 4, OCC = 1, GM = 1;
 };
 template <> struct GemmCfgNarrow<float> {
-  static constexpr int BM = 128, BN = 64, BK = 16, WM = 32, WN = 64, NW = 4, OCC = 1;
+  static constexpr int BM = 128, BN = 64, BK = 16, WM = 32, WN = 64, NW = 4, OCC = 1, GM = 1;
+};
+struct DlCfg {
+  static constexpr int BM = 256, BN = 256, BK = 64, WM = 128, WN = 64, NW = 8, OCC = 2, ST = 2,
+                       GM = 4;
 };
 
 template <typename T, class C, class Epi>
-static hipError_t launch(const T* A, long lda, const T* W, long ldw, int M, int N, int K, Epi epi,
-                         hipStream_t st) {
+static hipError_t launch_staged(const T* A, long lda, const T* W, long ldw, int M, int N, int K,
+                                Epi epi, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (K % C::BK != 0) return hipErrorInvalidValue;
+  if (K % C::BK != 0 || N % 4 != 0) return hipErrorInvalidValue;
   const long tiles = (long)cdiv(M, C::BM) * cdiv(N, C::BN);
-  hipLaunchKernelGGL((k_gemm<T, C::BM, C::BN, C::BK, C::WM, C::WN, C::NW, C::OCC, Epi>),
+  hipLaunchKernelGGL((k_gemm<T, C::BM, C::BN, C::BK, C::WM, C::WN, C::NW, C::OCC, C::GM, Epi>),
                      dim3((unsigned)tiles), dim3(64 * C::NW), 0, st, A, lda, W, ldw, M, N, K, epi);
   return hipGetLastError();
+}
+
+template <typename T, class Epi>
+static hipError_t launch(const T* A, long lda, const T* W, long ldw, int M, int N, int K, Epi epi,
+                         hipStream_t st) {
+  if constexpr (sizeof(T) == 2) {
+    typedef DlCfg C;
+    if (M <= 0 || N <= 0) return hipSuccess;
+    if (K % C::BK != 0 || N % 4 != 0) return hipErrorInvalidValue;
+    const long tiles = (long)cdiv(M, C::BM) * cdiv(N, C::BN);
+    hipLaunchKernelGGL((k_gemm_dl<C::BM, C::BN, C::BK, C::WM, C::WN, C::NW, C::OCC, C::ST, C::GM, Epi>),
+                       dim3((unsigned)tiles), dim3(64 * C::NW), 0, st, A, lda, W, ldw, M, N, K, epi);
+    return hipGetLastError();
+  } else {
+    return launch_staged<T, GemmCfg<T>>(A, lda, W, ldw, M, N, K, epi, st);
+  }
 }
 
 template <typename T>
 hipError_t gemm_store(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
                       int act, T* out, long ldo, hipStream_t st) {
   EpiStore<T> e{out, ldo, bias, act};
-  return launch<T, GemmCfg<T>>(A, lda, W, K, M, N, K, e, st);
+  return launch<T>(A, lda, W, K, M, N, K, e, st);
 }
 
 template <typename T>
 hipError_t gemm_store_t(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
                         T* out, long ldo, hipStream_t st) {
   EpiStoreT<T> e{out, ldo, bias};
-  return launch<T, GemmCfg<T>>(A, lda, W, K, M, N, K, e, st);
+  return launch<T>(A, lda, W, K, M, N, K, e, st);
 }
 
 template <typename T>
 hipError_t gemm_qkv(const T* A, const T* W, int M, int d, const float* bias, int L, T* qk, T* vt,
                     long vt_ld, hipStream_t st) {
   EpiQKV<T> e{qk, vt, bias, d, L, vt_ld, (long)d * vt_ld};
-  return launch<T, GemmCfg<T>>(A, d, W, d, M, 3 * d, d, e, st);
+  return launch<T>(A, d, W, d, M, 3 * d, d, e, st);
 }
 
 template <typename T>
 hipError_t gemm_residual(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
                          const float* gate, float* z, hipStream_t st) {
   EpiResidual e{z, N, bias, gate};
-  return launch<T, GemmCfg<T>>(A, lda, W, K, M, N, K, e, st);
+  return launch<T>(A, lda, W, K, M, N, K, e, st);
 }
 
 template <typename T>
 hipError_t gemm_patch(const T* A, const T* W, int M, int d, int P, const float* bias, float* z,
                       hipStream_t st) {
   EpiPatch e{z, d, bias};
-  return launch<T, GemmCfg<T>>(A, P, W, P, M, d, P, e, st);
+  return launch<T>(A, P, W, P, M, d, P, e, st);
 }
 
 template <typename T>
@@ -75,7 +93,7 @@ hipError_t gemm_head(const T* A, const T* W, int M, int d, int P, const float* b
                      const int* slot_id, int L, int gh, int gw, int F, int H, int Wd, long D,
                      hipStream_t st) {
   EpiHead e{out, slot_id, bias, L, gh, gw, F, H, Wd, D};
-  return launch<T, GemmCfgNarrow<T>>(A, d, W, d, M, P, d, e, st);
+  return launch_staged<T, GemmCfgNarrow<T>>(A, d, W, d, M, P, d, e, st);
 }
 
 #define CS_INST(T)                                                                              \

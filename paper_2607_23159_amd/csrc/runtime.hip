@@ -186,13 +186,13 @@ static cs_status validate_desc(const cs_model_desc* m) {
   CHECK(m->hidden == m->heads * m->head_dim, CS_E_INVAL, "hidden != heads * head_dim");
   CHECK(m->head_dim == 32 || m->head_dim == 64 || m->head_dim == 128, CS_E_UNSUPPORTED,
         "head_dim must be 32, 64 or 128");
-  CHECK(m->hidden % 64 == 0 && m->ffn % 64 == 0 && m->text_dim % 32 == 0, CS_E_UNSUPPORTED,
-        "hidden and ffn must be multiples of 64, text_dim of 32");
+  CHECK(m->hidden % 64 == 0 && m->ffn % 64 == 0 && m->text_dim % 64 == 0, CS_E_UNSUPPORTED,
+        "hidden, ffn and text_dim must be multiples of 64");
   CHECK(m->freq_dim == 256, CS_E_UNSUPPORTED, "freq_dim must be 256");
   CHECK(m->patch_t == 1 && m->patch_h == 2 && m->patch_w == 2, CS_E_UNSUPPORTED,
         "patch must be (1,2,2)");
   CHECK(m->lat_h % 2 == 0 && m->lat_w % 2 == 0, CS_E_INVAL, "lat_h and lat_w must be even");
-  CHECK((m->in_ch * 4) % 32 == 0, CS_E_UNSUPPORTED, "in_ch must be a multiple of 8");
+  CHECK((m->in_ch * 4) % 64 == 0, CS_E_UNSUPPORTED, "in_ch must be a multiple of 16");
   const long L = (long)m->lat_f * (m->lat_h / 2) * (m->lat_w / 2);
   CHECK(L <= (1L << 24), CS_E_UNSUPPORTED, "too many tokens");
   return CS_OK;
