@@ -46,12 +46,70 @@ __global__ __launch_bounds__(256) void k_layer_norm(const float* __restrict__ z,
   }
 }
 
+// Register-resident variant: the row (d = NV * 256) is read once as float4
+// chunks (lane-contiguous, so each wave access is 1 KB), reduced twice from
+// registers and written with one 8- or 16-byte store per chunk.
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void k_layer_norm_reg(const float* __restrict__ z, long rows,
+                                                         int d, const float* __restrict__ p0,
+                                                         const float* __restrict__ p1, int mode,
+                                                         T* __restrict__ u) {
+  const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float4* zr = reinterpret_cast<const float4*>(z + row * d);
+  float4 v[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) v[k] = zr[k * 64 + lane];
+  float s = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) s += (v[k].x + v[k].y) + (v[k].z + v[k].w);
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const float a = v[k].x - mean, b = v[k].y - mean, e = v[k].z - mean, f = v[k].w - mean;
+    q += (a * a + b * b) + (e * e + f * f);
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + 1e-6f);
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int col = 4 * (k * 64 + lane);
+    const float4 a = *reinterpret_cast<const float4*>(p0 + col);
+    const float4 b = *reinterpret_cast<const float4*>(p1 + col);
+    const float in[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+    const float pa[4] = {a.x, a.y, a.z, a.w}, pb[4] = {b.x, b.y, b.z, b.w};
+    float y[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float nv = (in[r] - mean) * rstd;
+      y[r] = mode == 0 ? nv * (1.0f + pb[r]) + pa[r] : nv * pa[r] + pb[r];
+    }
+    T* dst = u + row * d + col;
+    if constexpr (sizeof(T) == 2) {
+      bf16x4 o;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[r] = to_t<T>(y[r]);
+      *reinterpret_cast<bf16x4*>(dst) = o;
+    } else {
+      *reinterpret_cast<float4*>(dst) = make_float4(y[0], y[1], y[2], y[3]);
+    }
+  }
+}
+
 template <typename T>
 hipError_t layer_norm_mod(const float* z, long rows, int d, const float* p0, const float* p1,
                           int mode, T* u, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_layer_norm<T>, dim3((unsigned)cdiv(rows, 4)), dim3(256), 0, st, z, rows, d,
-                     p0, p1, mode, u);
+  const dim3 grid((unsigned)cdiv(rows, 4)), block(256);
+  switch (d % 256 == 0 ? d / 256 : 0) {
+#define CS_LN(NV) \
+  case NV: hipLaunchKernelGGL((k_layer_norm_reg<T, NV>), grid, block, 0, st, z, rows, d, p0, p1, mode, u); break;
+    CS_LN(1) CS_LN(2) CS_LN(3) CS_LN(4) CS_LN(6) CS_LN(8) CS_LN(12) CS_LN(16) CS_LN(20) CS_LN(24)
+#undef CS_LN
+    default:
+      hipLaunchKernelGGL(k_layer_norm<T>, grid, block, 0, st, z, rows, d, p0, p1, mode, u);
+  }
   return hipGetLastError();
 }
 
@@ -95,12 +153,100 @@ __global__ __launch_bounds__(256) void k_rmsnorm_rope(T* __restrict__ x, long ro
   }
 }
 
+// Register-resident variant: lane owns NV chunks of 8 consecutive channels
+// (4 RoPE pairs, 16 bytes in bf16); one read, one write per chunk.
+template <typename T> struct Vec8;
+template <> struct Vec8<bf16> {
+  typedef bf16x8 V;
+  static CS_DEV void get(const bf16* p, float* f) {
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = (float)v[i];
+  }
+  static CS_DEV void put(bf16* p, const float* f) {
+    bf16x8 v;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (bf16)f[i];
+    *reinterpret_cast<bf16x8*>(p) = v;
+  }
+};
+template <> struct Vec8<float> {
+  static CS_DEV void get(const float* p, float* f) {
+    const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+  static CS_DEV void put(float* p, const float* f) {
+    reinterpret_cast<float4*>(p)[0] = make_float4(f[0], f[1], f[2], f[3]);
+    reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
+  }
+};
+
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void k_rmsnorm_rope_reg(T* __restrict__ x, long rows, long ld,
+                                                           int d, int parts,
+                                                           const float* __restrict__ g0,
+                                                           const float* __restrict__ g1,
+                                                           const float2* __restrict__ rope, int L,
+                                                           int head_dim) {
+  const long item = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (item >= rows * parts) return;
+  const long row = item / parts;
+  const int part = (int)(item - row * parts);
+  T* xr = x + row * ld + (long)part * d;
+  const float* g = part == 0 ? g0 : g1;
+  float v[NV][8];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) Vec8<T>::get(xr + 8 * (k * 64 + lane), v[k]);
+  float s = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += v[k][i] * v[k][i];
+  const float r = 1.0f / sqrtf(wave_sum(s) / (float)d + 1e-6f);
+  const int tok = (int)(row % L);
+  const int hp = head_dim >> 1;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int c0 = 8 * (k * 64 + lane);
+    const float4 ga = *reinterpret_cast<const float4*>(g + c0);
+    const float4 gb = *reinterpret_cast<const float4*>(g + c0 + 4);
+    const float gg[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
+    float y[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) y[i] = v[k][i] * r * gg[i];
+    if (rope) {
+      const float4* t = reinterpret_cast<const float4*>(rope + (long)tok * hp + ((c0 >> 1) % hp));
+      const float4 t0 = t[0], t1 = t[1];
+      const float cs_[8] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w};
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const float a = y[2 * p], b = y[2 * p + 1], c = cs_[2 * p], sn = cs_[2 * p + 1];
+        y[2 * p] = a * c - b * sn;
+        y[2 * p + 1] = a * sn + b * c;
+      }
+    }
+    Vec8<T>::put(xr + c0, y);
+  }
+}
+
 template <typename T>
 hipError_t rmsnorm_rope(T* x, long rows, long ld, int d, int parts, const float* g0,
                         const float* g1, const float2* rope, int L, int head_dim, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_rmsnorm_rope<T>, dim3((unsigned)cdiv(rows * parts, 4)), dim3(256), 0, st, x,
-                     rows, ld, d, parts, g0, g1, rope, L, head_dim);
+  const dim3 grid((unsigned)cdiv(rows * parts, 4)), block(256);
+  switch (d % 512 == 0 ? d / 512 : 0) {
+#define CS_RR(NV)                                                                                \
+  case NV:                                                                                       \
+    hipLaunchKernelGGL((k_rmsnorm_rope_reg<T, NV>), grid, block, 0, st, x, rows, ld, d, parts, g0, \
+                       g1, rope, L, head_dim);                                                   \
+    break;
+    CS_RR(1) CS_RR(2) CS_RR(3) CS_RR(4) CS_RR(6) CS_RR(8) CS_RR(10) CS_RR(12)
+#undef CS_RR
+    default:
+      hipLaunchKernelGGL(k_rmsnorm_rope<T>, grid, block, 0, st, x, rows, ld, d, parts, g0, g1, rope,
+                         L, head_dim);
+  }
   return hipGetLastError();
 }
 
