@@ -269,241 +269,4 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash(AttnArgs<T> a) {
   }
 }
 
-// ---------------------------------------------------------------------------
-// Software-pipelined variant (one 32-query block per wave).  Iteration t
-// issues the score product of tile t+1 (matrix cores) before the softmax of
-// tile t (vector ALU), so the two are independent inside the wave and the
-// scheduler can interleave them; then O += V_t P_t.  K and V^T use separate
-// two-slot rings: iteration t reads K_{t+1} and V_t, and refills the slots of
-// K_t and V_{t-1} with K_{t+2} and V_{t+1} (prefetched into registers during
-// the iteration), so one barrier per iteration still suffices.
-// ---------------------------------------------------------------------------
-// SPLIT = 1: waves w and w + NW/2 (which share a SIMD) take the two halves
-// of an iteration in opposite order, so one runs its score MFMAs while the
-// other runs its softmax.  SPLIT = 2: one order for all waves, with an
-// explicit instruction interleave of the score MFMAs and the softmax.
-template <typename T, int DH, int KVT, int NW, int OCC, bool CROSS, int SPLIT = 1>
-__global__ __launch_bounds__(64 * NW, OCC) void k_flash_pp(AttnArgs<T> a) {
-  typedef Mfma32<T> MF;
-  constexpr int KPL = MF::KPL, KSTEP = MF::KSTEP;
-  constexpr int CH = 16 / (int)sizeof(T);
-  constexpr int KLD = DH + CH;
-  constexpr int VLD = KVT + CH;
-  constexpr int NKT = KVT / 32;
-  constexpr int NDT = DH / 32;
-  constexpr int NKS = DH / KSTEP;
-  constexpr int NPS = 32 / KSTEP;
-  constexpr int NT = 64 * NW;
-  constexpr int K_CH = KVT * DH / CH / NT;
-  constexpr int V_CH = DH * KVT / CH / NT;
-  static_assert(K_CH * CH * NT == KVT * DH && V_CH * CH * NT == DH * KVT, "tile split");
-
-  __shared__ __attribute__((aligned(16))) T sK[2][KVT * KLD];
-  __shared__ __attribute__((aligned(16))) T sV[2][DH * VLD];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int half = lane >> 5, l32 = lane & 31;
-  const int head = blockIdx.y, s = blockIdx.z;
-  const int kvs = a.kv_sel ? a.kv_sel[s] : s;
-  const int q0 = blockIdx.x * (NW * 32) + wave * 32;
-
-  const T* qb_ = a.q + (long)s * a.q_ss + head * DH;
-  const T* kb_ = a.k + (long)kvs * a.k_ss + head * DH;
-  const T* vb_ = a.vt + (long)kvs * a.vt_ss + (long)head * DH * a.vt_ld;
-
-  typename MF::frag qf[NKS];
-  {
-    const int row = min(q0 + l32, a.lq - 1);
-    const T* src = qb_ + (long)row * a.q_ld + KPL * half;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      qf[ks] = MF::load(src + ks * KSTEP);
-      asm volatile("" : "+v"(qf[ks]));
-    }
-  }
-
-  Chunk16 rk[K_CH], rv[V_CH];
-  auto load_k = [&](int kv0) {
-#pragma unroll
-    for (int c = 0; c < K_CH; ++c) {
-      const int id = c * NT + tid;
-      const int r = id / (DH / CH), cc = id % (DH / CH);
-      rk[c] = ld16(kb_ + (long)min(kv0 + r, a.lk - 1) * a.k_ld + cc * CH);
-    }
-  };
-  auto store_k = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < K_CH; ++c) {
-      const int id = c * NT + tid;
-      const int r = id / (DH / CH), cc = id % (DH / CH);
-      st16(&sK[buf][r * KLD + cc * CH], rk[c]);
-    }
-  };
-  auto load_v = [&](int kv0) {
-#pragma unroll
-    for (int c = 0; c < V_CH; ++c) {
-      const int id = c * NT + tid;
-      const int r = id / (KVT / CH), cc = id % (KVT / CH);
-      rv[c] = ld16(vb_ + (long)r * a.vt_ld + kv0 + cc * CH);
-    }
-  };
-  auto store_v = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < V_CH; ++c) {
-      const int id = c * NT + tid;
-      const int r = id / (KVT / CH), cc = id % (KVT / CH);
-      const T* src = reinterpret_cast<const T*>(&rv[c]);
-#pragma unroll
-      for (int g = 0; g < CH / 4; ++g) {
-        const int key = cc * CH + 4 * g;
-        const int w = key & 31;
-        const int pos = (key & ~31) + 16 * ((w >> 2) & 1) + 4 * (w >> 3);
-        T* dst = &sV[buf][r * VLD + pos];
-        if (sizeof(T) == 2)
-          *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(src + 4 * g);
-        else
-          *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src + 4 * g);
-      }
-    }
-  };
-  auto scores = [&](int buf, f32x16* sc) {
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sc[kt][r] = 0.0f;
-    const T* pk = &sK[buf][l32 * KLD + KPL * half];
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
-        sc[kt] = MF::mma(MF::load(pk + kt * 32 * KLD + ks * KSTEP), qf[ks], sc[kt]);
-  };
-
-  f32x16 o[NDT];
-#pragma unroll
-  for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[dt][r] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
-
-  const int ntiles = (a.lk + KVT - 1) / KVT;
-  load_k(0);
-  store_k(0);
-  load_v(0);
-  store_v(0);
-  if (ntiles > 1) {
-    load_k(KVT);
-    store_k(1);
-  }
-  __syncthreads();
-  f32x16 s_cur[NKT];
-  scores(0, s_cur);
-
-  const bool late = SPLIT == 1 && wave >= NW / 2;
-  for (int t = 0; t < ntiles; ++t) {
-    const bool has_next = t + 1 < ntiles;
-    if (t + 2 < ntiles) load_k((t + 2) * KVT);
-    if (has_next) load_v((t + 1) * KVT);
-    f32x16 s_next[NKT];
-    // The next tile's scores are formed even on the last iteration (from the
-    // stale, finite K slot) and discarded, so that the block is branch free.
-    if (!late) scores((t + 1) & 1, s_next);
-
-    // softmax of tile t
-    const int kv0 = t * KVT;
-    if (kv0 + KVT > a.lk) {
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (kv0 + kt * 32 + acc_row(r, lane) >= a.lk) s_cur[kt][r] = -INFINITY;
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kt][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * a.scale_log2;
-    if (__any(mx > m_run + RESCALE_LOG2)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-    }
-    typename MF::frag pf[NKT][NPS];
-    float lsum = 0.0f;
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) {
-      float p[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(s_cur[kt][r], a.scale_log2, -m_run));
-#pragma unroll
-      for (int ps = 0; ps < NPS; ++ps) {
-        if constexpr (KPL == 1) {
-          pf[kt][ps] = to_t<T>(p[ps]);
-          lsum += p[ps];
-        } else {
-          typename MF::frag f;
-#pragma unroll
-          for (int i = 0; i < KPL; ++i) f[i] = to_t<T>(p[ps * KPL + i]);
-          pf[kt][ps] = f;
-          const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
-#pragma unroll
-          for (int i = 0; i < KPL; i += 2) {
-            const bf16x2 pr = {f[i], f[i + 1]};
-            lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, one, lsum, false);
-          }
-        }
-      }
-    }
-    l_run += lsum;
-
-    // O^T += V_t^T P_t^T
-    const T* pv = &sV[t & 1][l32 * VLD + 16 * half];
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-      for (int ps = 0; ps < NPS; ++ps)
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-          o[dt] = MF::mma(MF::load(pv + dt * 32 * VLD + kt * 32 + ps * KPL), pf[kt][ps], o[dt]);
-    if (SPLIT == 2) {
-      // interleave: each score MFMA (with its fragment read) followed by a
-      // slice of the softmax arithmetic
-#pragma unroll
-      for (int i = 0; i < NKS * NKT; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
-      }
-    }
-    if (late) scores((t + 1) & 1, s_next);
-
-    if (t + 2 < ntiles) store_k(t & 1);
-    if (has_next) store_v((t + 1) & 1);
-    __syncthreads();
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) s_cur[kt] = s_next[kt];
-  }
-
-  const float l_tot = l_run + __shfl_xor(l_run, 32, WAVE);
-  const float inv = 1.0f / l_tot;
-  const int row = q0 + l32;
-  if (row < a.lq) {
-    T* dst = a.o + (long)s * a.o_ss + (long)row * a.o_ld + head * DH;
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int ch = dt * 32 + 8 * g + 4 * half;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) dst[ch + r] = to_t<T>(o[dt][4 * g + r] * inv);
-      }
-  }
-}
-
 }  // namespace cs
