@@ -41,6 +41,7 @@ def parse():
     p.add_argument("--cfg", action="store_true", help="two guidance branches (w = 5.0)")
     p.add_argument("--fp32", action="store_true", help="fp32 transformer arithmetic")
     p.add_argument("--reference", action="store_true", help="also run the full rollouts for rho")
+    p.add_argument("--tau-sweep", default="", help="comma-separated extra tau values, one rollout each")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true", help="no per-kernel HIP event timing")
     return p.parse_args()
@@ -90,6 +91,10 @@ def cpu_baseline(model_cfg, computed_per_cand_step: float, n_branch: int):
                        f"B={n_branch})")}
 
 
+def progress(msg: str) -> None:
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -114,18 +119,22 @@ def main():
                              n_steps=args.n_steps, tau=args.tau)
     m, r = wl.model, wl.roll
     gen_s = time.perf_counter() - t_gen
+    progress(f"inputs generated ({gen_s:.1f} s); uploading weights")
     gm = GpuModel(m, wl.weights)
     inp = Inputs(wl)
+    progress("model ready")
     wl.weights = None
     N, T = r.n_cand, r.n_steps
     S = N * nb
 
-    def rollout(mode=None, timed_profile=False):
+    def rollout(mode=None, label="cached"):
         desc = B.RolloutDesc(r, wl.timesteps, **({} if mode is None else {"mode": mode}))
         h = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[1] if nb == 2 else None)
         try:
             for k in range(1, T + 1):
                 B.cs_denoise_step(h, k)
+                if k % 10 == 0:
+                    progress(f"{label} rollout: step {k}/{T}")
             scores = B.cs_score(h, inp.w, N)
             st = B.cs_rollout_stats(h)
             return scores, int(st.computed), int(st.calls)
@@ -138,11 +147,15 @@ def main():
     torch.cuda.synchronize()
 
     ref_scores = None
+    full_s = None
     if args.reference:
-        ref_scores, _, _ = rollout(mode=synth.CACHE_OFF)
+        torch.cuda.synchronize()
+        t_ref = time.perf_counter()
+        ref_scores, _, _ = rollout(mode=synth.CACHE_OFF, label="full reference")
+        full_s = time.perf_counter() - t_ref
 
     for _ in range(args.warmup):
-        rollout()
+        rollout(label="warmup")
     torch.cuda.synchronize()
 
     if not args.no_profile:
@@ -153,7 +166,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        scores, c, n = rollout()
+        scores, c, n = rollout(label="timed")
         computed += c
         calls += n
         if ref_scores is not None:
@@ -189,8 +202,48 @@ def main():
         roof["gemm_tflops"] = round(gflops / (g_ms * 1e-3) / 1e12, 1) if g_ms > 0 else None
         roof["family_ms"] = {k: round(vv[0], 2) for k, vv in fam.items()}
 
+    # tau sweep (each value: one timed cached rollout, compared with the
+    # reference when it was run)
+    sweep = []
+    for tv in [float(x) for x in args.tau_sweep.split(",") if x.strip()]:
+        r_t = __import__("dataclasses").replace(r, tau=tv)
+        desc = B.RolloutDesc(r_t, wl.timesteps)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        h = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[1] if nb == 2 else None)
+        try:
+            for k in range(1, T + 1):
+                B.cs_denoise_step(h, k)
+                if k % 10 == 0:
+                    progress(f"tau={tv} rollout: step {k}/{T}")
+            sc = B.cs_score(h, inp.w, N)
+            st = B.cs_rollout_stats(h)
+        finally:
+            B.cs_rollout_free(h)
+        dt_s = time.perf_counter() - t1
+        rec = {"tau": tv, "candidate_steps_per_s": round(N * T / dt_s, 4),
+               "skip_fraction": round(1 - st.computed / st.calls, 4), "ms_per_rollout": round(dt_s * 1e3, 1)}
+        if ref_scores is not None:
+            _, _, rho_t, top1_t = B.cs_rank(sc, ref_scores)
+            rec.update({"rho_vs_full": rho_t, "top1_vs_full": top1_t,
+                        "regret": float(max(ref_scores) - ref_scores[int(np.argmax(sc))])})
+        sweep.append(rec)
+
+    # cost model (Sec. Method, cost analysis): per-rollout costs of the
+    # cached (C_c) and full (C_f) N-candidate batches, per candidate
+    costs = None
+    if full_s is not None:
+        cc = wall / args.steps / N
+        cf = full_s / N
+        gamma = cc / cf
+        costs = {"C_c_s": round(cc, 3), "C_f_s": round(cf, 3), "gamma": round(gamma, 4),
+                 "break_even_N": round(1.0 / (1.0 - gamma), 3) if gamma < 1 else None,
+                 "keep_s": round(N * cc, 2), "commit_s": round(N * cc + cf, 2),
+                 "best_of_N_full_s": round(N * cf, 2)}
+
     cpu = None
     if not args.no_cpu_baseline:
+        progress("timing the CPU oracle on a sample")
         try:
             cpu = cpu_baseline(m, computed / (N * T * args.steps), nb)
         except Exception as e:  # report, never hide
@@ -217,6 +270,8 @@ def main():
         "skip_fraction": round(1.0 - computed / max(calls, 1), 4),
         "rho_vs_full": rho,
         "top1_vs_full": top1,
+        "tau_sweep": sweep or None,
+        "costs": costs,
         "roofline": roof,
         "cpu_baseline": cpu,
         "input_gen_s": round(gen_s, 1),

@@ -115,6 +115,11 @@ MODELS: Dict[str, ModelCfg] = {
     "tiny": ModelCfg(n_blocks=2, hidden=128, heads=4, head_dim=32, ffn=512,
                      text_dim=128, text_len=32, in_ch=16, lat_f=4, lat_h=16,
                      lat_w=16, dtype=DTYPE_FP32),
+    # Ragged geometry: 3x9x11 = 297 tokens (no tile size divides it), 100-wide
+    # latent rows, 4 heads x 64.
+    "ragged": ModelCfg(n_blocks=2, hidden=256, heads=4, head_dim=64, ffn=512,
+                       text_dim=64, text_len=19, in_ch=16, lat_f=3, lat_h=18,
+                       lat_w=22, dtype=DTYPE_FP32),
     # Wan widths, 2 blocks, 384 tokens: full-width parity at oracle cost.
     "wan_mid": ModelCfg(n_blocks=2, hidden=1536, heads=12, head_dim=128,
                         ffn=8960, text_dim=4096, text_len=512, in_ch=16,
@@ -135,6 +140,8 @@ MODELS: Dict[str, ModelCfg] = {
 WORKLOADS: Dict[str, Tuple[str, RolloutCfg]] = {
     "tiny": ("tiny", RolloutCfg(n_cand=4, n_steps=10, k_warm=1, k_cool=1,
                                 tau=0.1)),
+    "ragged": ("ragged", RolloutCfg(n_cand=3, n_steps=8, k_warm=1, k_cool=1,
+                                    tau=0.1)),
     "wan_mid": ("wan_mid", RolloutCfg(n_cand=4, n_steps=10, k_warm=1,
                                       k_cool=1, tau=0.1)),
     "wan13b_full": ("wan13b", RolloutCfg(n_cand=1, n_steps=50,

@@ -103,3 +103,13 @@ def test_cs_rank_argument_errors():
         B.cs_rank([1.0, float("nan")], [2.0, 1.0])
     _, _, rho, _ = B.cs_rank([1.0, 1.0, 1.0], [1.0, 2.0, 3.0])
     assert math.isnan(rho)
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    import importlib
+    import subprocess
+    import sys
+    code = ("import paper_2607_23159_amd.binding as b; b.LIB_PATH = '/nonexistent/libcachedsearch.so'; "
+            "b._lib = None\ntry:\n    b.lib()\nexcept RuntimeError as e:\n    print('raised', e)\n")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT)
+    assert "raised" in out.stdout and "not built" in out.stdout

@@ -1,0 +1,149 @@
+"""GPU tests of the search layer and of the library's edge and error paths.
+
+Commit mode (Alg. 1, commit): regenerating the cached winner at full compute
+must reproduce that seed's full-compute latent bit for bit (the rollout is
+seed-deterministic and the kernels are batch-invariant).  Ragged geometry:
+297 tokens, 19 text tokens, head_dim 64.  State machine and allocation
+failures surface as status codes without touching later work."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from oracle import dit as odit
+from oracle import rollout as orl
+from paper_2607_23159_amd import binding as B
+from paper_2607_23159_amd import synth
+from paper_2607_23159_amd.search import GpuModel, Inputs, cached_search, run_rollout
+from parity import TOL, compare_schedules, oracle_masks, rel_l2
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
+def test_commit_reproduces_full_rollout_bitwise(dtype):
+    say(f"commit mode dtype={dtype}")
+    wl = synth.make_workload("tiny", n_branch=2, init="stress", dtype=dtype)
+    gm = GpuModel(wl.model, wl.weights)
+    res = cached_search(gm, wl, mode="commit", with_reference=True)
+    assert res.full is not None and res.order_full is not None
+    assert np.array_equal(res.delivered, res.full.latents[res.winner])
+    keep = cached_search(gm, wl, mode="keep", with_reference=False)
+    assert keep.winner == res.winner
+    assert np.array_equal(keep.delivered, res.cached.latents[res.winner])
+    # the host ranking agrees with the oracle's ranking function on the same scores
+    from oracle import rank as orank
+    oc, of, rho, top1, _ = orank.rank_report(list(res.cached.scores), list(res.full.scores))
+    assert oc == res.order_cached and of == res.order_full and top1 == res.top1
+    assert rho == pytest.approx(res.rho, abs=1e-12)
+    gm.close()
+
+
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
+def test_ragged_geometry_velocity_and_rollout(dtype):
+    say(f"ragged dtype={dtype}")
+    wl = synth.make_workload("ragged", n_branch=2, init="stress", dtype=dtype)
+    m = wl.model
+    assert m.tokens == 297
+    gm = GpuModel(m, wl.weights)
+    W = {k: v.astype(np.float64) for k, v in wl.named_weights().items()}
+    x = wl.noise
+    v = gm.velocity(torch.from_numpy(x.reshape(x.shape[0], -1)).cuda(), 0.6, torch.from_numpy(wl.ctx[1]).cuda())
+    v = v.cpu().numpy().reshape(x.shape)
+    emb = odit.text_embedding(wl.ctx[1], W)
+    for i in range(x.shape[0]):
+        # one evaluation: half the latent bar (bf16 rounding through two blocks)
+        assert rel_l2(v[i], odit.velocity(x[i], 0.6, emb, W, m)) < TOL[dtype] / 2
+    res = orl.run_workload(wl)
+    om, oa = oracle_masks(res, wl.roll.n_cand, 2, wl.roll.n_steps)
+    g = run_rollout(gm, wl)
+    exc = compare_schedules(g.masks, om, oa, wl.roll.tau)
+    if exc:
+        g = run_rollout(gm, wl, override=om)
+    for i in range(wl.roll.n_cand):
+        assert rel_l2(g.latents[i], res.latents[i]) < TOL[dtype]
+    gm.close()
+
+
+def test_single_candidate_rollout_and_batch_invariance_of_rollouts():
+    """Candidate i of an N-candidate rollout equals the 1-candidate rollout of
+    the same seed, bit for bit (cache on, two branches)."""
+    wl = synth.make_workload("tiny", n_branch=2, init="stress", dtype=synth.DTYPE_BF16)
+    gm = GpuModel(wl.model, wl.weights)
+    full = run_rollout(gm, wl, tau=0.1)
+    for i in (0, 3):
+        one = synth.Workload(wl.name, wl.model, wl.roll, wl.weights, wl.ctx, wl.noise[i:i + 1], wl.scorer,
+                             wl.timesteps)
+        g = run_rollout(gm, one, tau=0.1, n_cand=1)
+        assert np.array_equal(g.latents[0], full.latents[i])
+        assert np.array_equal(g.masks[:, :2], full.masks[:, 2 * i:2 * i + 2])
+    gm.close()
+
+
+def test_state_machine_errors():
+    wl = synth.make_workload("tiny", dtype=synth.DTYPE_FP32, init="stress")
+    gm = GpuModel(wl.model, wl.weights)
+    inp = Inputs(wl)
+    desc = B.RolloutDesc(wl.roll, wl.timesteps)
+    h = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], None)
+    try:
+        with pytest.raises(B.CsError) as e:
+            B.cs_denoise_step(h, 2)
+        assert e.value.status == B.CS_E_STATE
+        with pytest.raises(B.CsError) as e:
+            B.cs_denoise_step(h, 0)
+        assert e.value.status == B.CS_E_INVAL
+        B.cs_cache_decide(h, 1, wl.roll.n_cand)
+        with pytest.raises(B.CsError) as e:
+            B.cs_cache_decide(h, 1, wl.roll.n_cand)
+        assert e.value.status == B.CS_E_STATE
+        B.cs_denoise_step(h, 1)
+        st = B.cs_rollout_stats(h)
+        assert st.steps_done == 1 and st.computed == st.calls == wl.roll.n_cand
+    finally:
+        B.cs_rollout_free(h)
+    # rollout argument validation before device work
+    bad = B.RolloutDesc(wl.roll, wl.timesteps, tau=float("nan"))
+    with pytest.raises(B.CsError) as e:
+        B.cs_rollout_init(gm.h, bad, inp.x1, inp.ctx[0], None)
+    assert e.value.status == B.CS_E_INVAL
+    t = wl.timesteps.copy()
+    t[3] = t[2]
+    with pytest.raises(B.CsError) as e:
+        B.cs_rollout_init(gm.h, B.RolloutDesc(wl.roll, t), inp.x1, inp.ctx[0], None)
+    assert e.value.status == B.CS_E_INVAL
+    with pytest.raises(B.CsError) as e:
+        B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[0])
+    assert e.value.status == B.CS_E_INVAL
+    gm.close()
+
+
+def test_allocation_failure_is_reported_and_recoverable():
+    wl = synth.make_workload("tiny", dtype=synth.DTYPE_FP32, init="stress")
+    gm = GpuModel(wl.model, wl.weights)
+    inp = Inputs(wl)
+    desc = B.RolloutDesc(wl.roll, wl.timesteps)
+    lib = B.lib()
+    lib.cs_debug_set_alloc_cap(4096)
+    try:
+        with pytest.raises(B.CsError) as e:
+            B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], None)
+        assert e.value.status == B.CS_E_NOMEM
+    finally:
+        lib.cs_debug_set_alloc_cap(0)
+    g = run_rollout(gm, wl)   # the model is still usable afterwards
+    assert g.calls == wl.roll.n_cand * wl.roll.n_steps
+    gm.close()
