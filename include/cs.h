@@ -172,6 +172,23 @@ cs_status cs_denoise_step(cs_rollout* r, int32_t step);
  * scores: host [n_cand] double.  Synchronises. */
 cs_status cs_score(cs_rollout* r, const float* w, double* scores);
 
+/* Pruned composition (Sec. Composition with pruned search).
+ * cs_rollout_enable_preview(r, 1) makes every following cs_denoise_step also
+ * keep the guided velocity v~ of that step (one extra [n_cand][D] fp32
+ * buffer, allocated here; 0 frees it).  cs_preview_score then scores the
+ * sampler's x0 estimate after the last completed step k,
+ * x0_hat = x_{t_{k+1}} - t_{k+1} v~_k, as <w, x0_hat>/sqrt(D) (fp64, fixed
+ * order); it returns CS_E_STATE unless the preview was enabled before step
+ * k.  w: device [D]; scores: host [n_cand].  Synchronises.
+ * cs_rollout_retain keeps only the candidates keep[0..n_keep-1] (host,
+ * strictly increasing indices in the current numbering) with their complete
+ * cache state; they are renumbered 0..n_keep-1 and n_cand becomes n_keep.
+ * Not allowed between cs_cache_decide and cs_denoise_step (CS_E_STATE).
+ * Synchronises. */
+cs_status cs_rollout_enable_preview(cs_rollout* r, int32_t on);
+cs_status cs_preview_score(cs_rollout* r, const float* w, double* scores);
+cs_status cs_rollout_retain(cs_rollout* r, const int32_t* keep, int32_t n_keep);
+
 /* Copy the current latents to dst: device [n_cand][D] float32. */
 cs_status cs_rollout_latents(cs_rollout* r, float* dst);
 

@@ -29,7 +29,11 @@ Readings where the paper is silent:
   - a call whose ||x_ref|| is 0 computes;
   - both branches receive the latent x_{t_k} of the current step;
   - static mode with period k computes a step s (K_w < s <= T-K_c) iff
-    (s - K_w) is a multiple of k; other steps in that range reuse Delta.
+    (s - K_w) is a multiple of k; other steps in that range reuse Delta;
+  - the sampler's internal x0 estimate after step k (used for the preview
+    score of the pruned search, Sec. Composition with pruned search) is the
+    rectified-flow extrapolation x0_hat = x_{t_{k+1}} - t_{k+1} * v~_k, which
+    equals x_{t_k} - t_k * v~_k.
 """
 from __future__ import annotations
 
@@ -62,6 +66,7 @@ class RolloutResult:
     log: List[StepRecord]
     n_compute: int
     n_calls: int
+    x0_hat: Optional[np.ndarray] = None   # [N][...] x0 estimate after step `preview_step`
 
     def schedule(self, i: int, b: int) -> List[bool]:
         return [r.compute for r in self.log if r.i == i and r.b == b]
@@ -77,9 +82,12 @@ def is_forced(k: int, T: int, k_warm: int, k_cool: int, has_ref: bool, mode: int
 def cached_rollout_one(x1: np.ndarray, velocity_fns: Sequence[Callable[[np.ndarray, float], np.ndarray]],
                        timesteps: Sequence[float], *, tau: float, k_warm: int, k_cool: int,
                        guidance: float, mode: int = CACHE_ADAPTIVE, static_k: int = 2,
-                       cand: int = 0, log: Optional[List[StepRecord]] = None) -> np.ndarray:
+                       cand: int = 0, log: Optional[List[StepRecord]] = None,
+                       preview_step: Optional[int] = None, preview_out: Optional[list] = None) -> np.ndarray:
     """One candidate's rollout.  ``velocity_fns[b](x, t)`` is the transformer
-    call of guidance branch b (b = 0 conditional, b = 1 unconditional)."""
+    call of guidance branch b (b = 0 conditional, b = 1 unconditional).  With
+    ``preview_step`` = k, the x0 estimate after step k is appended to
+    ``preview_out``."""
     B = len(velocity_fns)
     T = len(timesteps) - 1
     x = dit.as64(x1).copy()
@@ -119,6 +127,8 @@ def cached_rollout_one(x1: np.ndarray, velocity_fns: Sequence[Callable[[np.ndarr
                 log.append(StepRecord(k, cand, b, a_seen, compute))
         vt = v[0] if B == 1 else v[1] + guidance * (v[0] - v[1])
         x = x + (t_next - t_k) * vt
+        if preview_step is not None and k == preview_step and preview_out is not None:
+            preview_out.append(x - t_next * vt)
     return x
 
 
@@ -131,16 +141,19 @@ def dit_velocity_fns(W: Dict[str, np.ndarray], cfg, ctx: Sequence[np.ndarray]):
 
 def cached_rollout(x1: np.ndarray, velocity_fns, timesteps, *, tau: float, k_warm: int,
                    k_cool: int, guidance: float = 5.0, mode: int = CACHE_ADAPTIVE,
-                   static_k: int = 2) -> RolloutResult:
+                   static_k: int = 2, preview_step: Optional[int] = None) -> RolloutResult:
     """N independent candidate rollouts, x1 [N][...]."""
     log: List[StepRecord] = []
     outs = []
+    prev: list = []
     for i in range(x1.shape[0]):
         outs.append(cached_rollout_one(x1[i], velocity_fns, timesteps, tau=tau, k_warm=k_warm,
                                        k_cool=k_cool, guidance=guidance, mode=mode,
-                                       static_k=static_k, cand=i, log=log))
+                                       static_k=static_k, cand=i, log=log,
+                                       preview_step=preview_step, preview_out=prev))
     n_comp = sum(1 for r in log if r.compute)
-    return RolloutResult(np.stack(outs), log, n_comp, len(log))
+    return RolloutResult(np.stack(outs), log, n_comp, len(log),
+                         np.stack(prev) if prev else None)
 
 
 def score(latents: np.ndarray, w: np.ndarray) -> np.ndarray:
@@ -151,7 +164,7 @@ def score(latents: np.ndarray, w: np.ndarray) -> np.ndarray:
 
 
 def run_workload(wl, *, tau: Optional[float] = None, mode: Optional[int] = None,
-                 n_cand: Optional[int] = None) -> RolloutResult:
+                 n_cand: Optional[int] = None, preview_step: Optional[int] = None) -> RolloutResult:
     """Oracle rollout of a synthetic workload (see ``synth.make_workload``)."""
     from_cfg = wl.roll
     W = {k: v.astype(np.float64) for k, v in wl.named_weights().items()}
@@ -162,5 +175,21 @@ def run_workload(wl, *, tau: Optional[float] = None, mode: Optional[int] = None,
                           k_warm=from_cfg.k_warm, k_cool=from_cfg.k_cool,
                           guidance=from_cfg.guidance,
                           mode=from_cfg.mode if mode is None else mode,
-                          static_k=from_cfg.static_k)
+                          static_k=from_cfg.static_k, preview_step=preview_step)
+
+
+def pruned_search(wl, *, prune_step: int, keep: int, tau: Optional[float] = None):
+    """Pruned composition (Sec. Composition with pruned search): all
+    candidates run cached to ``prune_step``, are scored on their x0 estimate,
+    the ``keep`` best continue to the end.  Candidates are independent, so the
+    survivors' trajectories are those of the unpruned cached rollout.
+    Returns (kept indices in candidate order, preview scores, final scores of
+    the kept candidates, winner index)."""
+    res = run_workload(wl, tau=tau, preview_step=prune_step)
+    prev = score(res.x0_hat, wl.scorer)
+    order = sorted(range(len(prev)), key=lambda i: (-prev[i], i))
+    kept = sorted(order[:keep])
+    final = score(res.latents[kept], wl.scorer)
+    winner = kept[sorted(range(len(kept)), key=lambda j: (-final[j], j))[0]]
+    return kept, prev, final, winner, res
 

@@ -73,6 +73,9 @@ def lib() -> C.CDLL:
         "cs_score": (i32, [vp, pf, pd]),
         "cs_rollout_latents": (i32, [vp, pf]),
         "cs_rollout_stats": (i32, [vp, C.POINTER(cs_rollout_stats_t)]),
+        "cs_rollout_enable_preview": (i32, [vp, i32]),
+        "cs_preview_score": (i32, [vp, pf, pd]),
+        "cs_rollout_retain": (i32, [vp, pi32, i32]),
         "cs_rollout_export": (i32, [vp, vp, C.POINTER(sz)]),
         "cs_rollout_import": (i32, [vp, vp, sz]),
         "cs_rank": (i32, [pd, pd, i32, pi32, pi32, pd, pi32]),
@@ -194,6 +197,21 @@ def cs_score(r: int, w, n_cand: int) -> np.ndarray:
 
 def cs_rollout_latents(r: int, dst) -> None:
     _check(lib().cs_rollout_latents(r, _ptr(dst)))
+
+
+def cs_rollout_enable_preview(r: int, on: bool = True) -> None:
+    _check(lib().cs_rollout_enable_preview(r, 1 if on else 0))
+
+
+def cs_preview_score(r: int, w, n_cand: int) -> np.ndarray:
+    out = np.zeros(n_cand, np.float64)
+    _check(lib().cs_preview_score(r, _ptr(w), out.ctypes.data_as(C.POINTER(C.c_double))))
+    return out
+
+
+def cs_rollout_retain(r: int, keep: Sequence[int]) -> None:
+    k = np.ascontiguousarray(np.asarray(keep, dtype=np.int32))
+    _check(lib().cs_rollout_retain(r, k.ctypes.data_as(C.POINTER(C.c_int32)), int(k.size)))
 
 
 def cs_rollout_stats(r: int) -> cs_rollout_stats_t:

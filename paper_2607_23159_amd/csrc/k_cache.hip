@@ -143,7 +143,7 @@ __global__ __launch_bounds__(256) void k_cache_update(float* __restrict__ x, flo
                                                        const float* __restrict__ vbuf,
                                                        const uint8_t* __restrict__ mask, int n_cand,
                                                        int n_branch, long D, float dt, float w,
-                                                       int store_state) {
+                                                       int store_state, float* __restrict__ vt_out) {
   const long D4 = D >> 2;
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long)n_cand * D4) return;
@@ -179,18 +179,21 @@ __global__ __launch_bounds__(256) void k_cache_update(float* __restrict__ x, flo
   float4 xn;
   xn.x = xv.x + dt * vt.x; xn.y = xv.y + dt * vt.y; xn.z = xv.z + dt * vt.z; xn.w = xv.w + dt * vt.w;
   *xp = xn;
+  if (vt_out) reinterpret_cast<float4*>(vt_out + (long)i * D)[j] = vt;
 }
 
 hipError_t cache_update(float* x, float* xref, float* delta, const float* vbuf, const uint8_t* mask,
                         int n_cand, int n_branch, long D, float dt, float guidance,
-                        int store_state, hipStream_t st) {
+                        int store_state, float* vt_out, hipStream_t st) {
   const long n = (long)n_cand * (D >> 2);
   hipLaunchKernelGGL(k_cache_update, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, x, xref, delta,
-                     vbuf, mask, n_cand, n_branch, D, dt, guidance, store_state);
+                     vbuf, mask, n_cand, n_branch, D, dt, guidance, store_state, vt_out);
   return hipGetLastError();
 }
 
+// Partial sums of <w, x - c*vt> (vt NULL: <w, x>).
 __global__ __launch_bounds__(256) void k_score_partials(const float* __restrict__ x,
+                                                         const float* __restrict__ vt, float c,
                                                          const float* __restrict__ w, long D,
                                                          double* __restrict__ partials) {
   __shared__ double sh[4];
@@ -202,7 +205,12 @@ __global__ __launch_bounds__(256) void k_score_partials(const float* __restrict_
   for (int k = 0; k < CHUNK_F4; ++k) {
     const long j = (long)chunk * (CHUNK / 4) + k * 256 + threadIdx.x;
     if (j < D4) {
-      const float4 a = xi[j], b = wv[j];
+      float4 a = xi[j];
+      const float4 b = wv[j];
+      if (vt) {
+        const float4 u = reinterpret_cast<const float4*>(vt + (long)i * D)[j];
+        a.x -= c * u.x; a.y -= c * u.y; a.z -= c * u.z; a.w -= c * u.w;
+      }
       acc += ((double)a.x * b.x + (double)a.y * b.y) + ((double)a.z * b.z + (double)a.w * b.w);
     }
   }
@@ -210,10 +218,10 @@ __global__ __launch_bounds__(256) void k_score_partials(const float* __restrict_
   if (threadIdx.x == 0) partials[(long)i * nchunk + chunk] = t;
 }
 
-hipError_t score_partials(const float* x, const float* w, int n_cand, long D, double* partials,
-                          hipStream_t st) {
+hipError_t score_partials(const float* x, const float* vt, float c, const float* w, int n_cand,
+                          long D, double* partials, hipStream_t st) {
   dim3 grid((unsigned)score_chunks(D), (unsigned)n_cand);
-  hipLaunchKernelGGL(k_score_partials, grid, dim3(256), 0, st, x, w, D, partials);
+  hipLaunchKernelGGL(k_score_partials, grid, dim3(256), 0, st, x, vt, c, w, D, partials);
   return hipGetLastError();
 }
 

@@ -92,13 +92,15 @@ hipError_t decide_finalize(const DecideParams& p, const double* partials, const 
                            int32_t* slot_list, int32_t* branch_list, DecideOut* out,
                            hipStream_t st);
 // x_i += dt * cfg(v_i0, v_i1); v_ib = vbuf (computed) or x + delta (skipped);
-// computed streams refresh delta and xref when store_state.
+// computed streams refresh delta and xref when store_state; the guided
+// velocity is also written to vt_out when it is not NULL.
 hipError_t cache_update(float* x, float* xref, float* delta, const float* vbuf,
                         const uint8_t* mask, int n_cand, int n_branch, long D, float dt,
-                        float guidance, int store_state, hipStream_t st);
+                        float guidance, int store_state, float* vt_out, hipStream_t st);
 int score_chunks(long D);
-hipError_t score_partials(const float* x, const float* w, int n_cand, long D, double* partials,
-                          hipStream_t st);
+// Partial sums of <w, x_i - c * vt_i> per 8192-element chunk (vt NULL: <w, x_i>).
+hipError_t score_partials(const float* x, const float* vt, float c, const float* w, int n_cand,
+                          long D, double* partials, hipStream_t st);
 hipError_t score_finalize(const double* partials, int n_cand, int nchunk, long D, double* scores,
                           hipStream_t st);
 

@@ -267,6 +267,8 @@ struct cs_rollout {
   long D = 0;
   int nchunk = 0, nschunk = 0;
   float *x = nullptr, *xref = nullptr, *delta = nullptr, *vbuf = nullptr, *wbuf = nullptr;
+  float* vtil = nullptr;      // guided velocity of the last step (preview only)
+  int vtil_step = -1;         // step whose guided velocity vtil holds
   double *a = nullptr, *partials = nullptr, *spart = nullptr, *scores = nullptr;
   uint8_t *has_ref = nullptr, *ovr = nullptr;
   int32_t *slots = nullptr, *branch = nullptr;
@@ -289,7 +291,7 @@ struct cs_rollout {
   ~cs_rollout() {
     ws.release();
     ctx.release();
-    void* ps[] = {x, xref, delta, vbuf, a, partials, spart, scores, has_ref, ovr, slots, branch, dec};
+    void* ps[] = {x, xref, delta, vbuf, vtil, a, partials, spart, scores, has_ref, ovr, slots, branch, dec};
     for (void* p : ps) if (p) hipFree(p);
     if (dec_host) hipHostFree(dec_host);
     if (ovr_host) hipHostFree(ovr_host);
@@ -796,7 +798,8 @@ static cs_status step_impl(cs_rollout* r, int32_t step) {
     ProfScope ps(m->prof, CS_K_UPDATE, st);
     const float dt = r->t[step] - r->t[step - 1];
     HIPC(cache_update(r->x, r->xref, r->delta, r->vbuf, r->mask_dev(), d.n_cand, d.n_branch, r->D, dt,
-                      d.guidance, d.mode != CS_CACHE_OFF ? 1 : 0, st));
+                      d.guidance, d.mode != CS_CACHE_OFF ? 1 : 0, r->vtil, st));
+    if (r->vtil) r->vtil_step = step;
   }
   r->calls += r->S;
   r->computed += r->n_compute;
@@ -814,12 +817,88 @@ cs_status cs_score(cs_rollout* r, const float* w, double* scores) {
     hipStream_t st = m->stream;
     {
       ProfScope ps(m->prof, CS_K_SCORE, st);
-      HIPC(score_partials(r->x, w, r->desc.n_cand, r->D, r->spart, st));
+      HIPC(score_partials(r->x, nullptr, 0.0f, w, r->desc.n_cand, r->D, r->spart, st));
       HIPC(score_finalize(r->spart, r->desc.n_cand, r->nschunk, r->D, r->scores, st));
     }
     HIPC(hipMemcpyAsync(r->scores_host, r->scores, r->desc.n_cand * sizeof(double), hipMemcpyDeviceToHost, st));
     HIPC(hipStreamSynchronize(st));
     memcpy(scores, r->scores_host, r->desc.n_cand * sizeof(double));
+    return CS_OK;
+  })
+}
+
+cs_status cs_rollout_enable_preview(cs_rollout* r, int32_t on) {
+  GUARD({
+    CHECK(r, CS_E_INVAL, "rollout is NULL");
+    if (on && !r->vtil) {
+      TRY(dmalloc((void**)&r->vtil, (size_t)r->desc.n_cand * r->D * sizeof(float)));
+      r->vtil_step = -1;
+    } else if (!on && r->vtil) {
+      HIPC(hipStreamSynchronize(r->model->stream));
+      HIPC(hipFree(r->vtil));
+      r->vtil = nullptr;
+      r->vtil_step = -1;
+    }
+    return CS_OK;
+  })
+}
+
+cs_status cs_preview_score(cs_rollout* r, const float* w, double* scores) {
+  GUARD({
+    CHECK(r, CS_E_INVAL, "rollout is NULL");
+    CHECK(w && scores, CS_E_INVAL, "w and scores must be non-NULL");
+    CHECK(r->vtil && r->vtil_step == r->steps_done && r->steps_done >= 1, CS_E_STATE,
+          "preview needs cs_rollout_enable_preview before the last completed step");
+    cs_model* m = r->model;
+    hipStream_t st = m->stream;
+    const float t_next = r->t[r->steps_done];
+    {
+      ProfScope ps(m->prof, CS_K_SCORE, st);
+      HIPC(score_partials(r->x, r->vtil, t_next, w, r->desc.n_cand, r->D, r->spart, st));
+      HIPC(score_finalize(r->spart, r->desc.n_cand, r->nschunk, r->D, r->scores, st));
+    }
+    HIPC(hipMemcpyAsync(r->scores_host, r->scores, r->desc.n_cand * sizeof(double), hipMemcpyDeviceToHost, st));
+    HIPC(hipStreamSynchronize(st));
+    memcpy(scores, r->scores_host, r->desc.n_cand * sizeof(double));
+    return CS_OK;
+  })
+}
+
+cs_status cs_rollout_retain(cs_rollout* r, const int32_t* keep, int32_t n_keep) {
+  GUARD({
+    CHECK(r && keep, CS_E_INVAL, "rollout and keep must be non-NULL");
+    const int N = r->desc.n_cand, B = r->desc.n_branch;
+    CHECK(n_keep >= 1 && n_keep <= N, CS_E_INVAL, "n_keep must be in [1, %d]", N);
+    for (int j = 0; j < n_keep; ++j) {
+      CHECK(keep[j] >= 0 && keep[j] < N, CS_E_INVAL, "keep[%d] = %d out of range", j, keep[j]);
+      CHECK(j == 0 || keep[j] > keep[j - 1], CS_E_INVAL, "keep must be strictly increasing");
+    }
+    CHECK(r->decided_step != r->steps_done + 1, CS_E_STATE,
+          "retain between cs_cache_decide and cs_denoise_step is not supported");
+    hipStream_t st = r->model->stream;
+    const size_t D = r->D;
+    // keep[j] >= j, so copying in increasing j never overwrites a source
+    // that a later copy still needs; the copies are ordered on the stream.
+    for (int j = 0; j < n_keep; ++j) {
+      const int i = keep[j];
+      if (i == j) continue;
+      HIPC(hipMemcpyAsync(r->x + j * D, r->x + i * D, D * 4, hipMemcpyDeviceToDevice, st));
+      if (r->vtil) HIPC(hipMemcpyAsync(r->vtil + j * D, r->vtil + i * D, D * 4, hipMemcpyDeviceToDevice, st));
+      HIPC(hipMemcpyAsync(r->xref + (size_t)j * B * D, r->xref + (size_t)i * B * D, B * D * 4,
+                          hipMemcpyDeviceToDevice, st));
+      HIPC(hipMemcpyAsync(r->delta + (size_t)j * B * D, r->delta + (size_t)i * B * D, B * D * 4,
+                          hipMemcpyDeviceToDevice, st));
+      HIPC(hipMemcpyAsync(r->a + (size_t)j * B, r->a + (size_t)i * B, B * sizeof(double),
+                          hipMemcpyDeviceToDevice, st));
+      HIPC(hipMemcpyAsync(r->has_ref + (size_t)j * B, r->has_ref + (size_t)i * B, B,
+                          hipMemcpyDeviceToDevice, st));
+      for (int b = 0; b < B; ++b) r->has_ref_h[j * B + b] = r->has_ref_h[i * B + b];
+    }
+    HIPC(hipStreamSynchronize(st));
+    r->desc.n_cand = n_keep;
+    r->S = n_keep * B;
+    r->has_ref_h.resize(r->S);
+    r->decided_step = 0;
     return CS_OK;
   })
 }

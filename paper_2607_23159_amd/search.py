@@ -151,3 +151,58 @@ def cached_search(model: GpuModel, wl: Workload, *, tau: Optional[float] = None,
     else:
         delivered = cached.latents[win]
     return SearchResult(win, oc, of, rho, top1, cached, full, delivered)
+
+
+@dataclasses.dataclass
+class PrunedResult:
+    kept: List[int]                # surviving candidates (original indices)
+    preview_scores: np.ndarray     # [N] scores of the x0 estimates at prune_step
+    final_scores: np.ndarray       # [len(kept)]
+    winner: int                    # original index
+    latents: np.ndarray            # [len(kept)][...] cached latents of the survivors
+    delivered: np.ndarray          # committed (full-compute) or kept latent of the winner
+    computed: int
+    calls: int
+
+
+def pruned_search(model: GpuModel, wl: Workload, *, prune_step: int, keep: int,
+                  tau: Optional[float] = None, mode: str = "commit") -> PrunedResult:
+    """Pruned composition (Sec. Composition with pruned search): run all N
+    candidates cached to ``prune_step``, score the x0 estimate, continue only
+    the ``keep`` best (cache state intact), rank them on their final latents,
+    then commit (regenerate the winner at full compute) or keep the draft."""
+    inp = Inputs(wl)
+    r = wl.roll
+    N, T = r.n_cand, r.n_steps
+    if not (1 <= prune_step < T and 1 <= keep <= N):
+        raise ValueError("need 1 <= prune_step < n_steps and 1 <= keep <= n_cand")
+    desc = B.RolloutDesc(r, wl.timesteps, **({} if tau is None else {"tau": tau}))
+    h = B.cs_rollout_init(model.h, desc, inp.x1, inp.ctx[0], inp.ctx[1] if r.n_branch == 2 else None)
+    try:
+        B.cs_rollout_enable_preview(h, True)
+        for k in range(1, prune_step + 1):
+            B.cs_denoise_step(h, k)
+        prev = B.cs_preview_score(h, inp.w, N)
+        order = sorted(range(N), key=lambda i: (-prev[i], i))
+        kept = sorted(order[:keep])
+        B.cs_rollout_retain(h, kept)
+        B.cs_rollout_enable_preview(h, False)
+        for k in range(prune_step + 1, T + 1):
+            B.cs_denoise_step(h, k)
+        final = B.cs_score(h, inp.w, keep)
+        lat = torch.empty_like(inp.x1[:keep])
+        B.cs_rollout_latents(h, lat)
+        st = B.cs_rollout_stats(h)
+        torch.cuda.synchronize()
+        lat_np = lat.cpu().numpy().reshape((keep,) + wl.noise.shape[1:])
+    finally:
+        B.cs_rollout_free(h)
+    j = sorted(range(keep), key=lambda q: (-final[q], q))[0]
+    win = kept[j]
+    if mode == "commit":
+        one = Workload(wl.name, wl.model, dataclasses.replace(r, n_cand=1), wl.weights, wl.ctx,
+                       wl.noise[win:win + 1], wl.scorer, wl.timesteps)
+        delivered = run_rollout(model, one, mode=CACHE_OFF).latents[0]
+    else:
+        delivered = lat_np[j]
+    return PrunedResult(kept, prev, final, win, lat_np, delivered, int(st.computed), int(st.calls))

@@ -147,3 +147,54 @@ def test_allocation_failure_is_reported_and_recoverable():
     g = run_rollout(gm, wl)   # the model is still usable afterwards
     assert g.calls == wl.roll.n_cand * wl.roll.n_steps
     gm.close()
+
+
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
+def test_pruned_search_matches_oracle(dtype):
+    """Pruned composition: survivors, preview scores and winner agree with
+    the oracle; survivors' latents equal the unpruned cached rollout's bit
+    for bit (retaining candidates does not perturb them)."""
+    from paper_2607_23159_amd.search import pruned_search
+    say(f"pruned search dtype={dtype}")
+    wl = synth.make_workload("tiny", n_branch=2, init="stress", dtype=dtype, n_cand=4)
+    gm = GpuModel(wl.model, wl.weights)
+    res = pruned_search(gm, wl, prune_step=4, keep=2, mode="commit")
+    kept, prev, final, winner, ores = orl.pruned_search(wl, prune_step=4, keep=2)
+    tol = TOL[dtype]
+    np.testing.assert_allclose(res.preview_scores, prev, rtol=0, atol=tol * np.abs(prev).max())
+    gap = np.min(np.diff(np.sort(prev)))
+    if res.kept != kept:
+        assert gap <= 4 * np.abs(res.preview_scores - prev).max(), (res.kept, kept)
+    else:
+        unpruned = run_rollout(gm, wl)
+        for j, i in enumerate(kept):
+            assert np.array_equal(res.latents[j], unpruned.latents[i])
+            assert rel_l2(res.latents[j], ores.latents[i]) < tol
+        assert res.winner == winner
+        full = run_rollout(gm, wl, mode=synth.CACHE_OFF)
+        assert np.array_equal(res.delivered, full.latents[res.winner])
+    # retained rollouts do fewer transformer calls than the unpruned search
+    assert res.calls < wl.roll.n_cand * wl.roll.n_steps * 2
+    gm.close()
+
+
+def test_retain_and_preview_argument_errors():
+    wl = synth.make_workload("tiny", dtype=synth.DTYPE_FP32, init="stress")
+    gm = GpuModel(wl.model, wl.weights)
+    inp = Inputs(wl)
+    h = B.cs_rollout_init(gm.h, B.RolloutDesc(wl.roll, wl.timesteps), inp.x1, inp.ctx[0], None)
+    try:
+        B.cs_denoise_step(h, 1)
+        with pytest.raises(B.CsError) as e:
+            B.cs_preview_score(h, inp.w, wl.roll.n_cand)    # preview not enabled
+        assert e.value.status == B.CS_E_STATE
+        for bad in ([1, 0], [0, 0], [5], []):
+            with pytest.raises(B.CsError) as e:
+                B.cs_rollout_retain(h, bad)
+            assert e.value.status == B.CS_E_INVAL
+        B.cs_rollout_retain(h, [1, 3])
+        B.cs_denoise_step(h, 2)
+        assert B.cs_rollout_stats(h).steps_done == 2
+    finally:
+        B.cs_rollout_free(h)
+    gm.close()

@@ -136,3 +136,24 @@ def test_rollout_deterministic(tiny_b2):
     a = R.run_workload(tiny_b2, n_cand=1)
     b = R.run_workload(tiny_b2, n_cand=1)
     assert np.array_equal(a.latents, b.latents)
+
+
+def test_x0_estimate_closed_form():
+    """Constant velocity c: x_{k+1} = x_1 - (1 - t_{k+1}) c and the x0 estimate
+    x_{k+1} - t_{k+1} c equals x_1 - c at every step (the exact endpoint)."""
+    x1 = synth.make_latent_batch((2, 2, 4, 4), seed=21)
+    c = 0.37
+    for k in (1, 4, 7):
+        res = R.cached_rollout(x1, [lambda x, t: np.full_like(x, c)], _grid(8), tau=0.0, k_warm=1, k_cool=1,
+                               guidance=1.0, mode=R.CACHE_OFF, preview_step=k)
+        np.testing.assert_allclose(res.x0_hat, x1.astype(np.float64) - c, rtol=1e-12, atol=1e-12)
+
+
+def test_pruned_search_keeps_top_preview_and_matches_unpruned(tiny_b2):
+    kept, prev, final, winner, res = R.pruned_search(tiny_b2, prune_step=4, keep=2)
+    order = sorted(range(len(prev)), key=lambda i: (-prev[i], i))
+    assert kept == sorted(order[:2])
+    full = R.run_workload(tiny_b2)
+    np.testing.assert_array_equal(res.latents, full.latents)   # preview does not perturb
+    np.testing.assert_allclose(final, R.score(full.latents[kept], tiny_b2.scorer))
+    assert winner in kept
