@@ -314,24 +314,29 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
     if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     const bf16* sa = smem + (kt % STAGES) * STAGE;
     const bf16* sb = sa + BM * BK;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+    // fragments of k-step ks+1 are requested before the products of ks
+    typename MF::frag fa[2][TM], fb[2][TN];
+    auto fetch = [&](int ks, int slot) {
       const int c = 2 * ks + half;
-      typename MF::frag fa[TM], fb[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = a_row0 + i * 32;
-        fa[i] = MF::load(sa + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+        fa[slot][i] = MF::load(sa + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int r = b_row0 + j * 32;
-        fb[j] = MF::load(sb + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+        fb[slot][j] = MF::load(sb + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
       }
+    };
+    fetch(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) fetch(ks + 1, (ks + 1) & 1);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = MF::mma(fb[j], fa[i], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = MF::mma(fb[ks & 1][j], fa[ks & 1][i], acc[i][j]);
     }
   }
 
@@ -367,16 +372,15 @@ template <typename T> CS_DEV void store4(T* p, const float* y) {
     *reinterpret_cast<float4*>(p) = make_float4(y[0], y[1], y[2], y[3]);
   }
 }
-CS_DEV float4 load_bias4(const float* b, int col0) {
-  return b ? *reinterpret_cast<const float4*>(b + col0) : make_float4(0.f, 0.f, 0.f, 0.f);
-}
+// Every GEMM of the model has a bias vector.
+CS_DEV float4 load_bias4(const float* b, int col0) { return *reinterpret_cast<const float4*>(b + col0); }
 
-template <typename T> struct EpiStore {
-  T* out; long ldo; const float* bias; int act;  // act: 0 none, 1 tanh-GELU
+template <typename T, int ACT> struct EpiStore {  // ACT: 0 none, 1 tanh-GELU
+  T* out; long ldo; const float* bias;
   CS_DEV void operator()(int row, int col0, const float* v) const {
-    const float4 b = load_bias4(bias, col0);
+    const float4 b = *reinterpret_cast<const float4*>(bias + col0);
     float y[4] = {v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w};
-    if (act == 1) {
+    if constexpr (ACT == 1) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) y[r] = gelu_tanh(y[r]);
     }
@@ -414,12 +418,13 @@ template <typename T> struct EpiStoreT {
   }
 };
 
-// Residual update z += gate * (acc + bias) (gate NULL: 1).
-struct EpiResidual {
+// Residual update z += gate * (acc + bias) (GATED = 0: gate 1).
+template <int GATED> struct EpiResidual {
   float* z; long ldz; const float* bias; const float* gate;
   CS_DEV void operator()(int row, int col0, const float* v) const {
     const float4 b = load_bias4(bias, col0);
-    const float4 g = gate ? *reinterpret_cast<const float4*>(gate + col0) : make_float4(1.f, 1.f, 1.f, 1.f);
+    float4 g = make_float4(1.f, 1.f, 1.f, 1.f);
+    if constexpr (GATED) g = *reinterpret_cast<const float4*>(gate + col0);
     float4* p = reinterpret_cast<float4*>(z + (long)row * ldz + col0);
     float4 o = *p;
     o.x += g.x * (v[0] + b.x);

@@ -56,8 +56,9 @@ static hipError_t launch(const T* A, long lda, const T* W, long ldw, int M, int 
 template <typename T>
 hipError_t gemm_store(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
                       int act, T* out, long ldo, hipStream_t st) {
-  EpiStore<T> e{out, ldo, bias, act};
-  return launch<T>(A, lda, W, K, M, N, K, e, st);
+  if (!bias) return hipErrorInvalidValue;
+  if (act == 1) return launch<T>(A, lda, W, K, M, N, K, EpiStore<T, 1>{out, ldo, bias}, st);
+  return launch<T>(A, lda, W, K, M, N, K, EpiStore<T, 0>{out, ldo, bias}, st);
 }
 
 template <typename T>
@@ -77,8 +78,9 @@ hipError_t gemm_qkv(const T* A, const T* W, int M, int d, const float* bias, int
 template <typename T>
 hipError_t gemm_residual(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
                          const float* gate, float* z, hipStream_t st) {
-  EpiResidual e{z, N, bias, gate};
-  return launch<T>(A, lda, W, K, M, N, K, e, st);
+  if (!bias) return hipErrorInvalidValue;
+  if (gate) return launch<T>(A, lda, W, K, M, N, K, EpiResidual<1>{z, N, bias, gate}, st);
+  return launch<T>(A, lda, W, K, M, N, K, EpiResidual<0>{z, N, bias, nullptr}, st);
 }
 
 template <typename T>

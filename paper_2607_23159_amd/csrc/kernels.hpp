@@ -5,7 +5,8 @@
 
 namespace cs {
 
-// ---- GEMM (k_gemm.hip).  W is [N][K] row-major (K contiguous).
+// ---- GEMM (k_gemm.hip).  W is [N][K] row-major (K contiguous); every
+// variant adds a bias vector (non-NULL) in its epilogue.
 template <typename T>
 hipError_t gemm_store(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
                       int act, T* out, long ldo, hipStream_t st);
