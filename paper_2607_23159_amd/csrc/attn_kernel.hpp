@@ -56,9 +56,15 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash(AttnArgs<T> a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
-  const int head = blockIdx.y, s = blockIdx.z;
+  // One flat grid over (query tile, head, stream), query tile fastest,
+  // taken XCD-contiguous: the workgroups resident on one XCD at a time work
+  // on the same head and read its K/V tiles through a shared L2.
+  const int n_qt = (a.lq + NW * QB * 32 - 1) / (NW * QB * 32);
+  const int vid = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int qt = vid % n_qt, hs = vid / n_qt;
+  const int head = hs % a.heads, s = hs / a.heads;
   const int kvs = a.kv_sel ? a.kv_sel[s] : s;
-  const int q0 = blockIdx.x * (NW * QB * 32) + wave * QB * 32;
+  const int q0 = qt * (NW * QB * 32) + wave * QB * 32;
 
   const T* qb_ = a.q + (long)s * a.q_ss + head * DH;
   const T* kb_ = a.k + (long)kvs * a.k_ss + head * DH;

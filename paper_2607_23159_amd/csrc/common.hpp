@@ -82,5 +82,14 @@ CS_DEV double wave_sum(double v) {
   return v;
 }
 
+// The dispatcher deals workgroups round-robin to the 8 XCDs, each with its
+// own L2.  This maps a hardware workgroup id to a virtual id so that every
+// XCD runs one contiguous range of virtual ids (a bijection on [0, nwg) for
+// any nwg); consecutive virtual ids then share their operands in one L2.
+CS_DEV int xcd_contiguous(int bid, int nwg) {
+  const int per = nwg >> 3, rem = nwg & 7, x = bid & 7;
+  return x * per + min(x, rem) + (bid >> 3);
+}
+
 inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 inline long round_up(long a, long b) { return (a + b - 1) / b * b; }

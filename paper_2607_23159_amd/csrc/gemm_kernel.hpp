@@ -60,8 +60,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
   const int tiles_n = (N + BN - 1) / BN;
   const int tiles_m = (M + BM - 1) / BM;
   const int nwg = gridDim.x;
-  int bid = blockIdx.x;
-  if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  const int bid = xcd_contiguous(blockIdx.x, nwg);
   int tm_i, tn_i;
   if (GM > 1) {
     const int group = bid / (GM * tiles_n);
@@ -238,8 +237,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   const int tiles_n = (N + BN - 1) / BN;
   const int tiles_m = (M + BM - 1) / BM;
   const int nwg = gridDim.x;
-  int bid = blockIdx.x;
-  if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  const int bid = xcd_contiguous(blockIdx.x, nwg);
   int tm_i, tn_i;
   if (GM > 1) {
     const int group = bid / (GM * tiles_n);

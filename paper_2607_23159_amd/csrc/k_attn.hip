@@ -11,7 +11,9 @@ int attn_kv_tile(int dtype_bytes, int head_dim) {
 template <typename T, int DH, int QB, int KVT, int NW, int OCC>
 static hipError_t launch_flash(const AttnArgs<T>& a, hipStream_t st) {
   const int qpw = NW * QB * 32;
-  dim3 grid((unsigned)cdiv(a.lq, qpw), (unsigned)a.heads, (unsigned)a.n_streams);
+  const long nwg = (long)cdiv(a.lq, qpw) * a.heads * a.n_streams;
+  if (nwg * 64 * NW > 0xFFFFFFFFL) return hipErrorInvalidConfiguration;
+  dim3 grid((unsigned)nwg);
   if (a.kv_sel)
     hipLaunchKernelGGL((k_flash<T, DH, QB, KVT, NW, OCC, true>), grid, dim3(64 * NW), 0, st, a);
   else
