@@ -244,6 +244,27 @@ def main():
         gflops = evals * (2.0 * L * m.n_blocks * (3 * d * d + 3 * d * d + 2 * d * F) + 4.0 * L * d * m.patch_dim)
         roof["gemm_tflops"] = round(gflops / (g_ms * 1e-3) / 1e12, 1) if g_ms > 0 else None
         roof["family_ms"] = {k: round(vv[0], 2) for k, vv in fam.items()}
+        # streaming kernels against the HBM roofline, algorithmic bytes:
+        # decision reads x and every branch's x_ref on each step past the
+        # forced windows; the fused update reads and writes x, reads v (or
+        # Delta when skipped) per stream and writes Delta, x_ref per computed
+        # stream; scoring reads x and w per candidate
+        D = int(np.prod(wl.noise.shape[1:]))
+        K = args.steps
+        adaptive = r.mode == synth.CACHE_ADAPTIVE
+        dec_launches = (T - r.k_warm - r.k_cool) * K if adaptive else 0
+        stream_bytes = {
+            "decide": 4.0 * D * N * (1 + nb) * dec_launches,
+            "update": 4.0 * D * (2 * N * T * K + S * T * K + (2 * computed if r.mode != synth.CACHE_OFF else 0)),
+            "score": 8.0 * D * N * K,
+        }
+        roof["streaming"] = {}
+        for name, nbytes in stream_bytes.items():
+            ms, n = fam[name]
+            gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 and nbytes > 0 else None
+            roof["streaming"][name] = {"bytes": nbytes, "ms": round(ms, 3), "calls": n,
+                                       "GB/s": None if gbs is None else round(gbs, 1),
+                                       "frac": None if gbs is None else round(gbs / PEAK_HBM_GBS, 4)}
 
     # tau sweep (each value: one timed cached rollout, compared with the
     # reference when it was run)

@@ -35,6 +35,84 @@ struct GemmShape {
   static_assert(A_CH * NT == BM * CPR && B_CH * NT == BN * CPR, "slice split");
 };
 
+// Accumulator layout shared by both kernels: the products are formed as C^T
+// tiles (W fragment as the MFMA A operand), so accumulator (i, j) of a lane
+// holds row i*32 + lane%32 of the wave's sub-tile and, in register 4g + r,
+// column j*32 + 8g + 4(lane/32) + r.  Every group of 4 registers is 4
+// consecutive columns of one row, i.e. one vector access in the epilogue.
+//
+// Every projection of the model has a bias; the accumulators start from it
+// (each column's bias, then the products in a fixed K order), so the
+// epilogue reads no bias.
+template <int TM, int TN>
+CS_DEV void init_acc_bias(f32x16 (&acc)[TM][TN], const float* __restrict__ bias, int col_base,
+                          int lane, int N) {
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int col0 = col_base + j * 32 + 8 * g + 4 * (lane >> 5);
+      float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (col0 < N) b = *reinterpret_cast<const float4*>(bias + col0);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        acc[i][j][4 * g] = b.x;
+        acc[i][j][4 * g + 1] = b.y;
+        acc[i][j][4 * g + 2] = b.z;
+        acc[i][j][4 * g + 3] = b.w;
+      }
+    }
+}
+
+// Epilogue over the wave's accumulators, in chunks of one accumulator (4
+// groups of 4 columns).  The operands an epilogue reads (Epi::pre: residual
+// and gate) are requested one chunk ahead of the chunk being stored, so their
+// latency overlaps the previous chunk's arithmetic and stores instead of
+// stalling every group.  A wave whose sub-tile lies inside [0,M) x [0,N)
+// (all but the tail tiles) takes a copy without bounds checks: straight-line
+// code lets the compiler wait for exactly the loads it needs, where branches
+// around each access would make it wait for all outstanding memory traffic.
+template <bool CHECK, int TM, int TN, class Epi>
+CS_DEV void gemm_epilogue_impl(const f32x16 (&acc)[TM][TN], int row_base, int col_base, int lane,
+                               int M, int N, const Epi& epi) {
+  constexpr int NQ = TM * TN;
+  typename Epi::Pre pre[2][4];
+  auto fetch = [&](int q, int slot) {
+    const int i = q / TN, j = q % TN;
+    const int row = row_base + i * 32 + (lane & 31);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int col0 = col_base + j * 32 + 8 * g + 4 * (lane >> 5);
+      if (!CHECK || (row < M && col0 < N)) pre[slot][g] = epi.pre(row, col0);
+    }
+  };
+  fetch(0, 0);
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    if (q + 1 < NQ) fetch(q + 1, (q + 1) & 1);
+    const int i = q / TN, j = q % TN;
+    const int row = row_base + i * 32 + (lane & 31);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int col0 = col_base + j * 32 + 8 * g + 4 * (lane >> 5);
+      if (!CHECK || (row < M && col0 < N)) {
+        const float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                            acc[i][j][4 * g + 3]};
+        epi(row, col0, v, pre[q & 1][g]);
+      }
+    }
+  }
+}
+
+template <int TM, int TN, class Epi>
+CS_DEV void gemm_epilogue(const f32x16 (&acc)[TM][TN], int row_base, int col_base, int lane,
+                          int M, int N, const Epi& epi) {
+  if (row_base + TM * 32 <= M && col_base + TN * 32 <= N)
+    gemm_epilogue_impl<false>(acc, row_base, col_base, lane, M, N, epi);
+  else
+    gemm_epilogue_impl<true>(acc, row_base, col_base, lane, M, N, epi);
+}
+
 // OCC = waves per SIMD the register budget is sized for; GM = tile-rows per
 // group of the tile order (1 = row-major).
 template <typename T, int BM, int BN, int BK, int WM, int WN, int NWAVE, int OCC, int GM, class Epi>
@@ -99,12 +177,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
   }
 
   f32x16 acc[S::TM][S::TN];
-#pragma unroll
-  for (int i = 0; i < S::TM; ++i)
-#pragma unroll
-    for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  init_acc_bias(acc, epi.bias, n0 + wn * WN, lane, N);
 
   const int nk = K / BK;
 #pragma unroll
@@ -163,24 +236,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
     __syncthreads();
   }
 
-  // epilogue: the products were formed as C^T tiles (W fragment as the MFMA A
-  // operand), so each lane owns, per accumulator, one row and 4 groups of 4
-  // consecutive columns; every group becomes one vector access.
-#pragma unroll
-  for (int i = 0; i < S::TM; ++i) {
-    const int row = m0 + wm * WM + i * 32 + (lane & 31);
-    if (row >= M) continue;
-#pragma unroll
-    for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int col0 = n0 + wn * WN + j * 32 + 8 * g + 4 * (lane >> 5);
-        if (col0 >= N) continue;
-        const float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                            acc[i][j][4 * g + 3]};
-        epi(row, col0, v);
-      }
-  }
+  gemm_epilogue(acc, m0 + wm * WM, n0 + wn * WN, lane, M, N, epi);
 }
 
 // ---------------------------------------------------------------------------
@@ -286,12 +342,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   };
 
   f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  init_acc_bias(acc, epi.bias, n0 + wn * WN, lane, N);
 
   const int nk = K / BK;
 #pragma unroll
@@ -338,28 +389,13 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
     }
   }
 
-  // epilogue: the products were formed as C^T tiles (W fragment as the MFMA A
-  // operand), so each lane owns, per accumulator, one row and 4 groups of 4
-  // consecutive columns; every group becomes one vector access.
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int row = m0 + wm * WM + i * 32 + (lane & 31);
-    if (row >= M) continue;
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int col0 = n0 + wn * WN + j * 32 + 8 * g + 4 * (lane >> 5);
-        if (col0 >= N) continue;
-        const float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                            acc[i][j][4 * g + 3]};
-        epi(row, col0, v);
-      }
-  }
+  gemm_epilogue(acc, m0 + wm * WM, n0 + wn * WN, lane, M, N, epi);
 }
 
 // ------------------------------------------------------------- epilogues
-// Called per (row, 4 consecutive columns col0..col0+3); N is a multiple of 4.
+// Each epilogue is called per (row, 4 consecutive columns col0..col0+3) with
+// the accumulated values v (bias included); N is a multiple of 4.  `Pre` is
+// what it reads from memory besides v, fetched ahead by `pre`.
 template <typename T> CS_DEV void store4(T* p, const float* y) {
   if constexpr (sizeof(T) == 2) {
     bf16x4 q;
@@ -370,14 +406,14 @@ template <typename T> CS_DEV void store4(T* p, const float* y) {
     *reinterpret_cast<float4*>(p) = make_float4(y[0], y[1], y[2], y[3]);
   }
 }
-// Every GEMM of the model has a bias vector.
-CS_DEV float4 load_bias4(const float* b, int col0) { return *reinterpret_cast<const float4*>(b + col0); }
+struct NoPre {};
 
 template <typename T, int ACT> struct EpiStore {  // ACT: 0 none, 1 tanh-GELU
   T* out; long ldo; const float* bias;
-  CS_DEV void operator()(int row, int col0, const float* v) const {
-    const float4 b = *reinterpret_cast<const float4*>(bias + col0);
-    float y[4] = {v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w};
+  typedef NoPre Pre;
+  CS_DEV Pre pre(int, int) const { return {}; }
+  CS_DEV void operator()(int row, int col0, const float* v, const Pre&) const {
+    float y[4] = {v[0], v[1], v[2], v[3]};
     if constexpr (ACT == 1) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) y[r] = gelu_tanh(y[r]);
@@ -391,16 +427,16 @@ template <typename T, int ACT> struct EpiStore {  // ACT: 0 none, 1 tanh-GELU
 // vT[stream][channel][token] with a padded token stride.
 template <typename T> struct EpiQKV {
   T* qk; T* vt; const float* bias; int d; int L; long vt_ld; long vt_ss;
-  CS_DEV void operator()(int row, int col0, const float* v) const {
-    const float4 b = load_bias4(bias, col0);
-    const float y[4] = {v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w};
+  typedef NoPre Pre;
+  CS_DEV Pre pre(int, int) const { return {}; }
+  CS_DEV void operator()(int row, int col0, const float* v, const Pre&) const {
     if (col0 < 2 * d) {
-      store4<T>(qk + (long)row * (2 * d) + col0, y);
+      store4<T>(qk + (long)row * (2 * d) + col0, v);
     } else {
       const int s = row / L, tok = row - s * L;
       T* dst = vt + (long)s * vt_ss + (long)(col0 - 2 * d) * vt_ld + tok;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) dst[(long)r * vt_ld] = to_t<T>(y[r]);
+      for (int r = 0; r < 4; ++r) dst[(long)r * vt_ld] = to_t<T>(v[r]);
     }
   }
 };
@@ -408,38 +444,42 @@ template <typename T> struct EpiQKV {
 // Transposed store of a single-stream projection: out[col][row].
 template <typename T> struct EpiStoreT {
   T* out; long ldo; const float* bias;
-  CS_DEV void operator()(int row, int col0, const float* v) const {
-    const float4 b = load_bias4(bias, col0);
-    const float y[4] = {v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w};
+  typedef NoPre Pre;
+  CS_DEV Pre pre(int, int) const { return {}; }
+  CS_DEV void operator()(int row, int col0, const float* v, const Pre&) const {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) out[(long)(col0 + r) * ldo + row] = to_t<T>(y[r]);
+    for (int r = 0; r < 4; ++r) out[(long)(col0 + r) * ldo + row] = to_t<T>(v[r]);
   }
 };
 
 // Residual update z += gate * (acc + bias) (GATED = 0: gate 1).
 template <int GATED> struct EpiResidual {
   float* z; long ldz; const float* bias; const float* gate;
-  CS_DEV void operator()(int row, int col0, const float* v) const {
-    const float4 b = load_bias4(bias, col0);
-    float4 g = make_float4(1.f, 1.f, 1.f, 1.f);
-    if constexpr (GATED) g = *reinterpret_cast<const float4*>(gate + col0);
-    float4* p = reinterpret_cast<float4*>(z + (long)row * ldz + col0);
-    float4 o = *p;
-    o.x += g.x * (v[0] + b.x);
-    o.y += g.y * (v[1] + b.y);
-    o.z += g.z * (v[2] + b.z);
-    o.w += g.w * (v[3] + b.w);
-    *p = o;
+  struct Pre { float4 z, g; };
+  CS_DEV Pre pre(int row, int col0) const {
+    Pre p;
+    p.z = *reinterpret_cast<const float4*>(z + (long)row * ldz + col0);
+    p.g = make_float4(1.f, 1.f, 1.f, 1.f);
+    if constexpr (GATED) p.g = *reinterpret_cast<const float4*>(gate + col0);
+    return p;
+  }
+  CS_DEV void operator()(int row, int col0, const float* v, const Pre& p) const {
+    float4 o = p.z;
+    o.x += p.g.x * v[0];
+    o.y += p.g.y * v[1];
+    o.z += p.g.z * v[2];
+    o.w += p.g.w * v[3];
+    *reinterpret_cast<float4*>(z + (long)row * ldz + col0) = o;
   }
 };
 
 // Patch embedding: z = acc + bias (fp32 residual stream).
 struct EpiPatch {
   float* z; long ldz; const float* bias;
-  CS_DEV void operator()(int row, int col0, const float* v) const {
-    const float4 b = load_bias4(bias, col0);
-    *reinterpret_cast<float4*>(z + (long)row * ldz + col0) =
-        make_float4(v[0] + b.x, v[1] + b.y, v[2] + b.z, v[3] + b.w);
+  typedef NoPre Pre;
+  CS_DEV Pre pre(int, int) const { return {}; }
+  CS_DEV void operator()(int row, int col0, const float* v, const Pre&) const {
+    *reinterpret_cast<float4*>(z + (long)row * ldz + col0) = make_float4(v[0], v[1], v[2], v[3]);
   }
 };
 
@@ -449,15 +489,16 @@ struct EpiPatch {
 // output latent is out + slot_id[slot] * D.
 struct EpiHead {
   float* out; const int* slot_id; const float* bias; int L, gh, gw, F, H, Wd; long D;
-  CS_DEV void operator()(int row, int col0, const float* v) const {
-    const float4 b = load_bias4(bias, col0);
+  struct Pre { int slot; };
+  CS_DEV Pre pre(int row, int) const { return {slot_id[row / L]}; }
+  CS_DEV void operator()(int row, int col0, const float* v, const Pre& p) const {
     const int c = col0 >> 2;
-    const int s = row / L, tok = row - s * L;
+    const int tok = row % L;
     const int f = tok / (gh * gw), rem = tok - f * gh * gw;
     const int hh = rem / gw, ww = rem - hh * gw;
-    float* dst = out + (long)slot_id[s] * D + (((long)c * F + f) * H + 2 * hh) * Wd + 2 * ww;
-    *reinterpret_cast<float2*>(dst) = make_float2(v[0] + b.x, v[1] + b.y);
-    *reinterpret_cast<float2*>(dst + Wd) = make_float2(v[2] + b.z, v[3] + b.w);
+    float* dst = out + (long)p.slot * D + (((long)c * F + f) * H + 2 * hh) * Wd + 2 * ww;
+    *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
+    *reinterpret_cast<float2*>(dst + Wd) = make_float2(v[2], v[3]);
   }
 };
 
