@@ -201,37 +201,61 @@ def text_embedding(ctx: np.ndarray, W: Dict[str, np.ndarray]) -> np.ndarray:
 # ------------------------------------------------------------------ network
 def block_forward(z: np.ndarray, j: int, m6: np.ndarray, ctx_emb: np.ndarray,
                   ang: np.ndarray, W: Dict[str, np.ndarray], heads: int,
-                  rows: Optional[np.ndarray] = None) -> np.ndarray:
+                  rows: Optional[np.ndarray] = None,
+                  attn_io: Optional[dict] = None) -> np.ndarray:
     """One transformer block.  z [L][d] float64; returns the new residual.
 
     ``rows`` (optional) restricts the output to those token rows: keys and
     values of the self-attention still come from every token, all other
     operations are row-wise.  The result is then [len(rows)][d].
+
+    ``attn_io`` (optional) serves attention-output broadcasting: its entries
+    "self" and "cross" are either None (compute that attention branch) or a
+    [L][d] array used in place of the branch's output, where the output is
+    taken after the branch's output projection and before the self-attention
+    gate.  The outputs actually used are written back to "self_out" and
+    "cross_out".
     """
     p = f"blk{j}."
     d = z.shape[1]
     mod = m6.reshape(6, d) + as64(W[p + "mod"])
     sh1, sc1, g1, sh2, sc2, g2 = mod
+    reuse_self = attn_io.get("self") if attn_io is not None else None
+    reuse_cross = attn_io.get("cross") if attn_io is not None else None
+    if attn_io is not None and rows is not None:
+        raise ValueError("attention-output broadcasting needs every row")
 
     # self-attention
-    u = layer_norm(z) * (1.0 + sc1) + sh1
-    qkv = linear(u, W[p + "qkv_w"], W[p + "qkv_b"])
-    k = apply_rope(rms_norm(qkv[:, d:2 * d], W[p + "k_gain"]), ang, heads)
-    v = qkv[:, 2 * d:]
-    if rows is None:
-        zr, q_in, ang_q = z, qkv[:, :d], ang
+    if reuse_self is not None:
+        zr, y = z, as64(reuse_self)
     else:
-        zr, q_in, ang_q = z[rows], qkv[rows, :d], ang[rows]
-    q = apply_rope(rms_norm(q_in, W[p + "q_gain"]), ang_q, heads)
-    o = attention(q, k, v, heads)
-    zr = zr + g1 * linear(o, W[p + "o_w"], W[p + "o_b"])
+        u = layer_norm(z) * (1.0 + sc1) + sh1
+        qkv = linear(u, W[p + "qkv_w"], W[p + "qkv_b"])
+        k = apply_rope(rms_norm(qkv[:, d:2 * d], W[p + "k_gain"]), ang, heads)
+        v = qkv[:, 2 * d:]
+        if rows is None:
+            zr, q_in, ang_q = z, qkv[:, :d], ang
+        else:
+            zr, q_in, ang_q = z[rows], qkv[rows, :d], ang[rows]
+        q = apply_rope(rms_norm(q_in, W[p + "q_gain"]), ang_q, heads)
+        o = attention(q, k, v, heads)
+        y = linear(o, W[p + "o_w"], W[p + "o_b"])
+    zr = zr + g1 * y
+    if attn_io is not None:
+        attn_io["self_out"] = y
 
     # cross-attention to the text embedding
-    u = layer_norm(zr) * as64(W[p + "ca_ln_g"]) + as64(W[p + "ca_ln_b"])
-    q = rms_norm(linear(u, W[p + "caq_w"], W[p + "caq_b"]), W[p + "caq_gain"])
-    kc = rms_norm(linear(ctx_emb, W[p + "cak_w"], W[p + "cak_b"]), W[p + "cak_gain"])
-    vc = linear(ctx_emb, W[p + "cav_w"], W[p + "cav_b"])
-    zr = zr + linear(attention(q, kc, vc, heads), W[p + "cao_w"], W[p + "cao_b"])
+    if reuse_cross is not None:
+        yc = as64(reuse_cross)
+    else:
+        u = layer_norm(zr) * as64(W[p + "ca_ln_g"]) + as64(W[p + "ca_ln_b"])
+        q = rms_norm(linear(u, W[p + "caq_w"], W[p + "caq_b"]), W[p + "caq_gain"])
+        kc = rms_norm(linear(ctx_emb, W[p + "cak_w"], W[p + "cak_b"]), W[p + "cak_gain"])
+        vc = linear(ctx_emb, W[p + "cav_w"], W[p + "cav_b"])
+        yc = linear(attention(q, kc, vc, heads), W[p + "cao_w"], W[p + "cao_b"])
+    zr = zr + yc
+    if attn_io is not None:
+        attn_io["cross_out"] = yc
 
     # feed-forward
     u = layer_norm(zr) * (1.0 + sc2) + sh2
@@ -241,14 +265,16 @@ def block_forward(z: np.ndarray, j: int, m6: np.ndarray, ctx_emb: np.ndarray,
 
 
 def velocity(x: np.ndarray, t: float, ctx_emb: np.ndarray, W: Dict[str, np.ndarray],
-             cfg, last_block_rows: Optional[np.ndarray] = None) -> np.ndarray:
+             cfg, last_block_rows: Optional[np.ndarray] = None,
+             attn_io: Optional[Sequence[dict]] = None) -> np.ndarray:
     """v_theta(x, t, c) for one latent x [C][F][H][W] (float64 result).
 
     ``ctx_emb`` is the text embedding (output of :func:`text_embedding`).
     ``last_block_rows`` restricts the last block and the head to the given
     tokens; the result is then the head output [len(rows)][patch_dim] rather
     than a latent (used to check single-block models at full size on a
-    sample of tokens).
+    sample of tokens).  ``attn_io`` (one dict per block, see
+    :func:`block_forward`) reuses and reports attention outputs.
     """
     pt, ph, pw = cfg.patch_t, cfg.patch_h, cfg.patch_w
     e, m = time_embedding(t, W, cfg.freq_dim)
@@ -256,7 +282,8 @@ def velocity(x: np.ndarray, t: float, ctx_emb: np.ndarray, W: Dict[str, np.ndarr
     z = linear(patchify(as64(x), pt, ph, pw), W["patch_w"], W["patch_b"])
     for j in range(cfg.n_blocks):
         rows = last_block_rows if j == cfg.n_blocks - 1 else None
-        z = block_forward(z, j, m, ctx_emb, ang, W, cfg.heads, rows)
+        z = block_forward(z, j, m, ctx_emb, ang, W, cfg.heads, rows,
+                          None if attn_io is None else attn_io[j])
     hm = e[None, :] + as64(W["head_mod"])
     sh, sc = hm[0], hm[1]
     y = linear(layer_norm(z) * (1.0 + sc) + sh, W["head_w"], W["head_b"])

@@ -30,6 +30,16 @@ Readings where the paper is silent:
   - both branches receive the latent x_{t_k} of the current step;
   - static mode with period k computes a step s (K_w < s <= T-K_c) iff
     (s - K_w) is a multiple of k; other steps in that range reuse Delta;
+  - attention-output broadcasting (PAB, one of the published engines of
+    Sec. Ranking preservation across published caching methods and Table
+    tab:baselines; self range 2, cross range 6):
+    the cached quantity is each attention branch's output after its output
+    projection and before the self-attention gate, per block, stream and
+    branch; steps 1..K_w and T-K_c+1..T compute every attention; a step s
+    in between recomputes a branch with range r iff (s - K_w) is a multiple
+    of r (the phase of the static variant) or no output is stored yet, and
+    otherwise reuses the stored output (multiplied by the current step's
+    gate); every call of every step runs the rest of the transformer;
   - the sampler's internal x0 estimate after step k (used for the preview
     score of the pruned search, Sec. Composition with pruned search) is the
     rectified-flow extrapolation x0_hat = x_{t_{k+1}} - t_{k+1} * v~_k, which
@@ -45,7 +55,7 @@ import numpy as np
 
 from . import dit
 
-CACHE_OFF, CACHE_ADAPTIVE, CACHE_STATIC = 0, 1, 2
+CACHE_OFF, CACHE_ADAPTIVE, CACHE_STATIC, CACHE_PAB = 0, 1, 2, 3
 
 
 @dataclasses.dataclass
@@ -130,6 +140,62 @@ def cached_rollout_one(x1: np.ndarray, velocity_fns: Sequence[Callable[[np.ndarr
         if preview_step is not None and k == preview_step and preview_out is not None:
             preview_out.append(x - t_next * vt)
     return x
+
+
+def pab_computes(k: int, T: int, k_warm: int, k_cool: int, r: int, have: bool) -> bool:
+    """Whether step k recomputes an attention branch of broadcast range r."""
+    if k <= k_warm or k > T - k_cool or not have:
+        return True
+    return (k - k_warm) % r == 0
+
+
+def pab_rollout_one(x1: np.ndarray, W: Dict[str, np.ndarray], cfg, embs: Sequence[np.ndarray],
+                    timesteps: Sequence[float], *, r_self: int, r_cross: int, k_warm: int,
+                    k_cool: int, guidance: float, sched: Optional[list] = None) -> np.ndarray:
+    """One candidate's rollout with attention-output broadcasting: every
+    step evaluates the transformer for every guidance branch (Eq. cfg, Eq.
+    euler), reusing each block's stored attention outputs on the steps the
+    schedule marks.  ``sched`` collects (k, self computed, cross computed)."""
+    B = len(embs)
+    T = len(timesteps) - 1
+    x = dit.as64(x1).copy()
+    stored = [[{"self": None, "cross": None} for _ in range(cfg.n_blocks)] for _ in range(B)]
+    for k in range(1, T + 1):
+        t_k, t_next = float(timesteps[k - 1]), float(timesteps[k])
+        cs = pab_computes(k, T, k_warm, k_cool, r_self, stored[0][0]["self"] is not None)
+        cc = pab_computes(k, T, k_warm, k_cool, r_cross, stored[0][0]["cross"] is not None)
+        if sched is not None:
+            sched.append((k, cs, cc))
+        v = []
+        for b in range(B):
+            io = [{"self": None if cs else stored[b][j]["self"],
+                   "cross": None if cc else stored[b][j]["cross"]} for j in range(cfg.n_blocks)]
+            v.append(dit.as64(dit.velocity(x, t_k, embs[b], W, cfg, attn_io=io)))
+            for j in range(cfg.n_blocks):
+                stored[b][j]["self"] = io[j]["self_out"]
+                stored[b][j]["cross"] = io[j]["cross_out"]
+        vt = v[0] if B == 1 else v[1] + guidance * (v[0] - v[1])
+        x = x + (t_next - t_k) * vt
+    return x
+
+
+def pab_rollout(wl, *, n_cand: Optional[int] = None, r_self: Optional[int] = None,
+                r_cross: Optional[int] = None, W: Optional[Dict[str, np.ndarray]] = None):
+    """Oracle PAB rollouts of a synthetic workload's first ``n_cand`` seeds.
+    Returns (latents [N][...], schedule [(k, self computed, cross computed)])."""
+    r = wl.roll
+    if W is None:
+        W = {k: v.astype(np.float64) for k, v in wl.named_weights().items()}
+    embs = [dit.text_embedding(c, W) for c in wl.ctx[:r.n_branch]]
+    x1 = wl.noise if n_cand is None else wl.noise[:n_cand]
+    outs, sched = [], []
+    for i in range(x1.shape[0]):
+        outs.append(pab_rollout_one(x1[i], W, wl.model, embs, [float(t) for t in wl.timesteps],
+                                    r_self=r.pab_self if r_self is None else r_self,
+                                    r_cross=r.pab_cross if r_cross is None else r_cross,
+                                    k_warm=r.k_warm, k_cool=r.k_cool, guidance=r.guidance,
+                                    sched=sched if i == 0 else None))
+    return np.stack(outs), sched
 
 
 def dit_velocity_fns(W: Dict[str, np.ndarray], cfg, ctx: Sequence[np.ndarray]):

@@ -34,7 +34,7 @@ CTX_UNCOND_SEED = 2
 SCORER_SEED = 3
 NOISE_SEED0 = 100
 
-CACHE_OFF, CACHE_ADAPTIVE, CACHE_STATIC = 0, 1, 2
+CACHE_OFF, CACHE_ADAPTIVE, CACHE_STATIC, CACHE_PAB = 0, 1, 2, 3
 DTYPE_BF16, DTYPE_FP32 = 0, 1
 
 
@@ -99,6 +99,10 @@ class RolloutCfg:
     mode: int = CACHE_ADAPTIVE
     static_k: int = 2
     shift: float = 1.0
+    # attention-output broadcast ranges (CACHE_PAB): self- and cross-attention
+    # outputs are recomputed every pab_self / pab_cross steps
+    pab_self: int = 2
+    pab_cross: int = 6
 
 
 # --------------------------------------------------------------------------
