@@ -75,6 +75,11 @@ def parse():
     p.add_argument("--tau-sweep", default="", help="comma-separated extra tau values, one rollout each")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true", help="no per-kernel HIP event timing")
+    p.add_argument("--mode", choices=["adaptive", "static", "pab"], default="adaptive",
+                   help="reuse engine: the drift-indicator cache, the static schedule, or "
+                        "attention-output broadcasting")
+    p.add_argument("--pab-self", type=int, default=2, help="self-attention broadcast range")
+    p.add_argument("--pab-cross", type=int, default=6, help="cross-attention broadcast range")
     p.add_argument("--calibration-copy", type=int, default=0,
                    help="bytes of one plain device-to-device copy made before timing (a "
                         "known-size reference for HBM counter runs)")
@@ -149,8 +154,11 @@ def main():
     dtype = synth.DTYPE_FP32 if args.fp32 else synth.DTYPE_BF16
     nb = 2 if args.cfg else 1
     t_gen = time.perf_counter()
+    mode = {"adaptive": synth.CACHE_ADAPTIVE, "static": synth.CACHE_STATIC,
+            "pab": synth.CACHE_PAB}[args.mode]
     wl = synth.make_workload(args.workload, n_branch=nb, dtype=dtype, n_cand=args.n_cand,
-                             n_steps=args.n_steps, tau=args.tau)
+                             n_steps=args.n_steps, tau=args.tau, mode=mode,
+                             pab_self=args.pab_self, pab_cross=args.pab_cross)
     m, r = wl.model, wl.roll
     gen_s = time.perf_counter() - t_gen
     progress(f"inputs generated ({gen_s:.1f} s); uploading weights")
@@ -160,6 +168,8 @@ def main():
     wl.weights = None
     N, T = r.n_cand, r.n_steps
     S = N * nb
+
+    reused = [0, 0]   # self / cross attention reuses, accumulated by rollout()
 
     def rollout(mode=None, label="cached"):
         desc = B.RolloutDesc(r, wl.timesteps, **({} if mode is None else {"mode": mode}))
@@ -171,6 +181,8 @@ def main():
                     progress(f"{label} rollout: step {k}/{T}")
             scores = B.cs_score(h, inp.w, N)
             st = B.cs_rollout_stats(h)
+            reused[0] += int(st.self_reused)
+            reused[1] += int(st.cross_reused)
             return scores, int(st.computed), int(st.calls)
         finally:
             B.cs_rollout_free(h)
@@ -205,6 +217,7 @@ def main():
         B.cs_profile_reset(gm.h)
     computed = calls = 0
     rho = top1 = None
+    reused[0] = reused[1] = 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -228,10 +241,12 @@ def main():
 
     L, d = m.tokens, m.hidden
     evals = computed                                   # stream evaluations in the timed region
+    self_evals = computed - reused[0]                  # of which ran self-attention
+    cross_evals = computed - reused[1]                 # ... and cross-attention
     roof = None
     if fam:
         sa_ms, sa_n = fam["self_attn"]
-        flops = 4.0 * L * L * d * m.n_blocks * evals   # QK^T and PV, 2 flop per MAC
+        flops = 4.0 * L * L * d * m.n_blocks * self_evals   # QK^T and PV, 2 flop per MAC
         ach = flops / (sa_ms * 1e-3) / 1e12 if sa_ms > 0 else 0.0
         peak = PEAK_FP32_TFLOPS if args.fp32 else PEAK_BF16_TFLOPS
         roof = {"bound": "mfma", "kernel": "k_flash (self-attention)", "achieved": round(ach, 1),
@@ -241,21 +256,27 @@ def main():
                 "flop_per_launch": flops / max(sa_n, 1)}
         g_ms, g_n = fam["gemm"]
         F = m.ffn
-        gflops = evals * (2.0 * L * m.n_blocks * (3 * d * d + 3 * d * d + 2 * d * F) + 4.0 * L * d * m.patch_dim)
+        # QKV + out-projection (4 d^2) on self-attention evaluations, cross q +
+        # out-projection (2 d^2) on cross-attention evaluations, FFN (2 d F),
+        # patch embedding and head on every evaluation
+        gflops = (2.0 * L * m.n_blocks * (4 * d * d * self_evals + 2 * d * d * cross_evals + 2 * d * F * evals)
+                  + 4.0 * L * d * m.patch_dim * evals)
         roof["gemm_tflops"] = round(gflops / (g_ms * 1e-3) / 1e12, 1) if g_ms > 0 else None
         roof["family_ms"] = {k: round(vv[0], 2) for k, vv in fam.items()}
         # streaming kernels against the HBM roofline, algorithmic bytes:
         # decision reads x and every branch's x_ref on each step past the
         # forced windows; the fused update reads and writes x, reads v (or
-        # Delta when skipped) per stream and writes Delta, x_ref per computed
-        # stream; scoring reads x and w per candidate
+        # Delta when skipped) per stream and, when the cache keeps state,
+        # writes Delta, x_ref per computed stream; scoring reads x and w per
+        # candidate
         D = int(np.prod(wl.noise.shape[1:]))
         K = args.steps
         adaptive = r.mode == synth.CACHE_ADAPTIVE
         dec_launches = (T - r.k_warm - r.k_cool) * K if adaptive else 0
         stream_bytes = {
             "decide": 4.0 * D * N * (1 + nb) * dec_launches,
-            "update": 4.0 * D * (2 * N * T * K + S * T * K + (2 * computed if r.mode != synth.CACHE_OFF else 0)),
+            "update": 4.0 * D * (2 * N * T * K + S * T * K
+                                 + (2 * computed if r.mode in (synth.CACHE_ADAPTIVE, synth.CACHE_STATIC) else 0)),
             "score": 8.0 * D * N * K,
         }
         roof["streaming"] = {}
@@ -328,10 +349,17 @@ def main():
         "data": "synthetic",
         "config": {"workload": (f"{args.workload}: Wan-shaped DiT {m.n_blocks} blocks d={d} "
                                 f"{m.heads}x{m.head_dim} ffn={m.ffn}, {L} tokens, N={N} seeds, "
-                                f"T={T}, tau={r.tau}, B={nb}, random init"),
+                                f"T={T}, " + (f"PAB ranges self {r.pab_self} cross {r.pab_cross}"
+                                               if mode == synth.CACHE_PAB else
+                                               f"tau={r.tau}" if mode == synth.CACHE_ADAPTIVE else
+                                               f"static period {r.static_k}")
+                                + f", B={nb}, random init"),
                    "n_cand": N, "n_steps": T, "tau": r.tau, "n_branch": nb,
                    "cache_mode": r.mode},
         "skip_fraction": round(1.0 - computed / max(calls, 1), 4),
+        "attn_reuse_fraction": ({"self": round(reused[0] / max(calls, 1), 4),
+                                 "cross": round(reused[1] / max(calls, 1), 4)}
+                                if mode == synth.CACHE_PAB else None),
         "rho_vs_full": rho,
         "top1_vs_full": top1,
         "tau_sweep": sweep or None,

@@ -55,8 +55,20 @@ typedef enum { CS_BF16 = 0, CS_FP32 = 1 } cs_dtype;
 /* Cache modes.  OFF computes every call (recovers the uncached rollout
  * G(c,s)); ADAPTIVE applies the accumulated drift rule with threshold tau;
  * STATIC computes every static_k-th step between warmup and cooldown (the
- * uniform-schedule baseline of Sec. Method, properties paragraph). */
-typedef enum { CS_CACHE_OFF = 0, CS_CACHE_ADAPTIVE = 1, CS_CACHE_STATIC = 2 } cs_cache_mode;
+ * uniform-schedule baseline of Sec. Method, properties paragraph).
+ * PAB is attention-output broadcasting, one of the published engines the
+ * paper compares (Sec. Ranking preservation across published caching
+ * methods, Table tab:baselines): every call runs the transformer, but each
+ * block's self- and cross-attention output (after the output projection,
+ * before the self-attention gate) is recomputed only every
+ * pab_self_range / pab_cross_range steps and reused in between.  Steps
+ * 1..k_warm and n_steps-k_cool+1..n_steps recompute both; a step s in
+ * between recomputes a branch of range r iff (s - k_warm) % r == 0 or
+ * nothing is stored yet.  PAB keeps two [n_blocks][N*B][tokens][hidden]
+ * arrays of the compute type on the device. */
+typedef enum {
+  CS_CACHE_OFF = 0, CS_CACHE_ADAPTIVE = 1, CS_CACHE_STATIC = 2, CS_CACHE_PAB = 3
+} cs_cache_mode;
 
 /* Transformer shape.  The paper treats the velocity model v_theta(x, t, c)
  * as a black box (Sec. Preliminaries); the library implements a Wan-shaped
@@ -88,6 +100,8 @@ typedef struct {
   int32_t mode;                  /* cs_cache_mode */
   float tau, guidance;
   const float* timesteps;
+  int32_t pab_self_range;        /* >= 1, read in CS_CACHE_PAB mode only  */
+  int32_t pab_cross_range;       /* >= 1, read in CS_CACHE_PAB mode only  */
 } cs_rollout_desc;
 
 typedef struct cs_model cs_model;
@@ -98,6 +112,8 @@ typedef struct {
   int32_t steps_done;            /* last completed step (0 after init)     */
   int64_t calls;                 /* transformer calls requested (N*B*steps)*/
   int64_t computed;              /* calls evaluated by the transformer     */
+  int64_t self_reused;           /* PAB: calls that reused the stored      */
+  int64_t cross_reused;          /*   self / cross attention outputs       */
 } cs_rollout_stats_t;
 
 /* Kernel families timed by the optional profiler (cs_profile_*). */
@@ -142,7 +158,10 @@ cs_status cs_velocity(cs_model* model, const float* x, int32_t n, float t, const
  * every seed).  x1: device [n_cand][D] float32 initial noise (copied).
  * ctx_cond / ctx_uncond: device [text_len][text_dim] float32; ctx_uncond
  * must be non-NULL iff n_branch == 2 (copied into per-branch cross-attention
- * keys/values here, once per rollout).  All cache state is zeroed. */
+ * keys/values here, once per rollout).  All cache state is zeroed.  In
+ * CS_CACHE_PAB mode both ranges must be >= 1 (else CS_E_INVAL) and the two
+ * attention-output arrays are allocated here (CS_E_NOMEM if they do not
+ * fit). */
 cs_status cs_rollout_init(cs_model* model, const cs_rollout_desc* desc, const float* x1,
                           const float* ctx_cond, const float* ctx_uncond, cs_rollout** out);
 void cs_rollout_free(cs_rollout* r);
@@ -156,7 +175,8 @@ void cs_rollout_free(cs_rollout* r);
  * and reported.  mask_out: NULL or host [n_cand][n_branch] (1 = compute).
  * a_out: NULL or host [n_cand][n_branch], the indicator value compared with
  * tau at this step, NaN where the call was forced.  Calling it twice for
- * the same step returns CS_E_STATE. */
+ * the same step returns CS_E_STATE.  In CS_CACHE_PAB mode every call
+ * computes (mask all 1, a NaN) unless overridden. */
 cs_status cs_cache_decide(cs_rollout* r, int32_t step, const uint8_t* override_mask,
                           uint8_t* mask_out, double* a_out);
 
@@ -164,7 +184,10 @@ cs_status cs_cache_decide(cs_rollout* r, int32_t step, const uint8_t* override_m
  * refresh Delta = v - x and x_ref = x on them (Eq. delta), form x + Delta on
  * the skipped ones (Eq. skip), combine branches (Eq. cfg) and take the
  * Euler step (Eq. euler).  Runs cs_cache_decide(step, NULL, NULL, NULL)
- * first if it was not called for this step. */
+ * first if it was not called for this step.  In CS_CACHE_PAB mode the
+ * attention outputs follow the broadcast schedule described with
+ * cs_cache_mode; a replay override is then not allowed (CS_E_UNSUPPORTED
+ * from cs_cache_decide). */
 cs_status cs_denoise_step(cs_rollout* r, int32_t step);
 
 /* Scores s_i = <w, x_i> / sqrt(D) of the current latents, summed in fp64 in
@@ -183,8 +206,8 @@ cs_status cs_score(cs_rollout* r, const float* w, double* scores);
  * cs_rollout_retain keeps only the candidates keep[0..n_keep-1] (host,
  * strictly increasing indices in the current numbering) with their complete
  * cache state; they are renumbered 0..n_keep-1 and n_cand becomes n_keep.
- * Not allowed between cs_cache_decide and cs_denoise_step (CS_E_STATE).
- * Synchronises. */
+ * Not allowed between cs_cache_decide and cs_denoise_step (CS_E_STATE),
+ * nor in CS_CACHE_PAB mode (CS_E_UNSUPPORTED).  Synchronises. */
 cs_status cs_rollout_enable_preview(cs_rollout* r, int32_t on);
 cs_status cs_preview_score(cs_rollout* r, const float* w, double* scores);
 cs_status cs_rollout_retain(cs_rollout* r, const int32_t* keep, int32_t n_keep);
@@ -198,7 +221,8 @@ cs_status cs_rollout_stats(cs_rollout* r, cs_rollout_stats_t* out);
  * has_ref}.  cs_rollout_export with buf == NULL stores the required size in
  * *bytes; otherwise buf (host) must hold *bytes bytes.  cs_rollout_import
  * restores a state exported from a rollout with the same model and
- * description.  Both synchronise. */
+ * description.  Both synchronise.  Not available in CS_CACHE_PAB mode,
+ * whose state includes the attention-output arrays (CS_E_UNSUPPORTED). */
 cs_status cs_rollout_export(cs_rollout* r, void* buf, size_t* bytes);
 cs_status cs_rollout_import(cs_rollout* r, const void* buf, size_t bytes);
 

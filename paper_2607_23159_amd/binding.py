@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcachedse
 
 CS_OK, CS_E_INVAL, CS_E_NOMEM, CS_E_DEVICE, CS_E_STATE, CS_E_UNSUPPORTED = range(6)
 CS_BF16, CS_FP32 = 0, 1
-CS_CACHE_OFF, CS_CACHE_ADAPTIVE, CS_CACHE_STATIC = 0, 1, 2
+CS_CACHE_OFF, CS_CACHE_ADAPTIVE, CS_CACHE_STATIC, CS_CACHE_PAB = 0, 1, 2, 3
 (CS_K_SELF_ATTN, CS_K_CROSS_ATTN, CS_K_GEMM, CS_K_NORM, CS_K_DECIDE, CS_K_UPDATE, CS_K_SCORE,
  CS_K_OTHER) = range(8)
 KERNEL_FAMILIES = ["self_attn", "cross_attn", "gemm", "norm", "decide", "update", "score", "other"]
@@ -42,11 +42,13 @@ class cs_rollout_desc(C.Structure):
     _fields_ = [("n_cand", C.c_int32), ("n_steps", C.c_int32), ("n_branch", C.c_int32),
                 ("k_warm", C.c_int32), ("k_cool", C.c_int32), ("static_k", C.c_int32),
                 ("mode", C.c_int32), ("tau", C.c_float), ("guidance", C.c_float),
-                ("timesteps", C.POINTER(C.c_float))]
+                ("timesteps", C.POINTER(C.c_float)),
+                ("pab_self_range", C.c_int32), ("pab_cross_range", C.c_int32)]
 
 
 class cs_rollout_stats_t(C.Structure):
-    _fields_ = [("steps_done", C.c_int32), ("calls", C.c_int64), ("computed", C.c_int64)]
+    _fields_ = [("steps_done", C.c_int32), ("calls", C.c_int64), ("computed", C.c_int64),
+                ("self_reused", C.c_int64), ("cross_reused", C.c_int64)]
 
 
 _lib: Optional[C.CDLL] = None
@@ -129,13 +131,15 @@ class RolloutDesc:
     def __init__(self, roll, timesteps: Sequence[float], **override):
         kw = dict(n_cand=roll.n_cand, n_steps=roll.n_steps, n_branch=roll.n_branch,
                   k_warm=roll.k_warm, k_cool=roll.k_cool, static_k=roll.static_k,
-                  mode=roll.mode, tau=roll.tau, guidance=roll.guidance)
+                  mode=roll.mode, tau=roll.tau, guidance=roll.guidance,
+                  pab_self=getattr(roll, "pab_self", 2), pab_cross=getattr(roll, "pab_cross", 6))
         kw.update(override)
         self.t = np.ascontiguousarray(np.asarray(timesteps, dtype=np.float32))
         self.c = cs_rollout_desc(kw["n_cand"], kw["n_steps"], kw["n_branch"], kw["k_warm"],
                                  kw["k_cool"], kw["static_k"], kw["mode"],
                                  float(kw["tau"]), float(kw["guidance"]),
-                                 self.t.ctypes.data_as(C.POINTER(C.c_float)))
+                                 self.t.ctypes.data_as(C.POINTER(C.c_float)),
+                                 int(kw["pab_self"]), int(kw["pab_cross"]))
 
 
 # ------------------------------------------------------------------- calls

@@ -473,6 +473,20 @@ template <int GATED> struct EpiResidual {
   }
 };
 
+// Residual update that also keeps the branch output y = acc + bias in y
+// (row stride N, compute type) for later reuse: z += gate * y.
+template <int GATED, typename T> struct EpiResidualStore {
+  float* z; long ldz; const float* bias; const float* gate; T* y;
+  typedef typename EpiResidual<GATED>::Pre Pre;
+  CS_DEV Pre pre(int row, int col0) const {
+    return EpiResidual<GATED>{z, ldz, bias, gate}.pre(row, col0);
+  }
+  CS_DEV void operator()(int row, int col0, const float* v, const Pre& p) const {
+    store4<T>(y + (long)row * ldz + col0, v);
+    EpiResidual<GATED>{z, ldz, bias, gate}(row, col0, v, p);
+  }
+};
+
 // Patch embedding: z = acc + bias (fp32 residual stream).
 struct EpiPatch {
   float* z; long ldz; const float* bias;

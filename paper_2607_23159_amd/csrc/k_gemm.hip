@@ -77,8 +77,12 @@ hipError_t gemm_qkv(const T* A, const T* W, int M, int d, const float* bias, int
 
 template <typename T>
 hipError_t gemm_residual(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
-                         const float* gate, float* z, hipStream_t st) {
+                         const float* gate, float* z, T* y, hipStream_t st) {
   if (!bias) return hipErrorInvalidValue;
+  if (y) {
+    if (gate) return launch<T>(A, lda, W, K, M, N, K, EpiResidualStore<1, T>{z, N, bias, gate, y}, st);
+    return launch<T>(A, lda, W, K, M, N, K, EpiResidualStore<0, T>{z, N, bias, nullptr, y}, st);
+  }
   if (gate) return launch<T>(A, lda, W, K, M, N, K, EpiResidual<1>{z, N, bias, gate}, st);
   return launch<T>(A, lda, W, K, M, N, K, EpiResidual<0>{z, N, bias, nullptr}, st);
 }
@@ -106,7 +110,7 @@ hipError_t gemm_head(const T* A, const T* W, int M, int d, int P, const float* b
   template hipError_t gemm_qkv<T>(const T*, const T*, int, int, const float*, int, T*, T*,     \
                                   long, hipStream_t);                                           \
   template hipError_t gemm_residual<T>(const T*, long, const T*, int, int, int, const float*,  \
-                                       const float*, float*, hipStream_t);                      \
+                                       const float*, float*, T*, hipStream_t);                  \
   template hipError_t gemm_patch<T>(const T*, const T*, int, int, int, const float*, float*,   \
                                     hipStream_t);                                               \
   template hipError_t gemm_head<T>(const T*, const T*, int, int, int, const float*, float*,    \

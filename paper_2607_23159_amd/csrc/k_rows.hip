@@ -364,6 +364,41 @@ hipError_t build_mods_strided(const float* m, const float* e, const float* table
   return hipGetLastError();
 }
 
+// ------------------------------------------------ stored-output reuse
+// z[r][c] += gate[c] * y[r][c] (gate NULL: 1), 8 consecutive channels per
+// thread: the residual update of an attention branch whose stored output is
+// reused instead of recomputed.
+template <typename T>
+__global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ z, const T* __restrict__ y,
+                                                      const float* __restrict__ gate, long n8,
+                                                      int d8) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  float yv[8], zv[8];
+  Vec8<T>::get(y + i * 8, yv);
+  Vec8<float>::get(z + i * 8, zv);
+  if (gate) {
+    float g[8];
+    Vec8<float>::get(gate + (i % d8) * 8, g);
+#pragma unroll
+    for (int r = 0; r < 8; ++r) zv[r] += g[r] * yv[r];
+  } else {
+#pragma unroll
+    for (int r = 0; r < 8; ++r) zv[r] += yv[r];
+  }
+  Vec8<float>::put(z + i * 8, zv);
+}
+
+template <typename T>
+hipError_t residual_add(float* z, const T* y, const float* gate, long rows, int d, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  if (d % 8 != 0) return hipErrorInvalidValue;
+  const long n8 = rows * d / 8;
+  hipLaunchKernelGGL(k_residual_add<T>, dim3((unsigned)cdiv(n8, 256)), dim3(256), 0, st, z, y, gate,
+                     n8, d / 8);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------- casts
 template <typename T>
 __global__ void k_cast(const float* __restrict__ s, T* __restrict__ d, long n) {
@@ -386,7 +421,8 @@ template <typename T> hipError_t cast_from_f32(const float* src, T* dst, long n,
                                   T*, hipStream_t);                                             \
   template hipError_t gemv<T>(const T*, const float*, const float*, int, int, int, float*,     \
                               hipStream_t);                                                     \
-  template hipError_t cast_from_f32<T>(const float*, T*, long, hipStream_t);
+  template hipError_t cast_from_f32<T>(const float*, T*, long, hipStream_t);                 \
+  template hipError_t residual_add<T>(float*, const T*, const float*, long, int, hipStream_t);
 CS_INST(bf16)
 CS_INST(float)
 #undef CS_INST

@@ -16,9 +16,11 @@ hipError_t gemm_store_t(const T* A, long lda, const T* W, int M, int N, int K, c
 template <typename T>
 hipError_t gemm_qkv(const T* A, const T* W, int M, int d, const float* bias, int L, T* qk, T* vt,
                     long vt_ld, hipStream_t st);
+// z[M][N] += gate * (A W^T + bias) (gate NULL: 1); when y is non-NULL the
+// branch output A W^T + bias is also stored to y[M][N] in the compute type.
 template <typename T>
 hipError_t gemm_residual(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
-                         const float* gate, float* z, hipStream_t st);
+                         const float* gate, float* z, T* y, hipStream_t st);
 template <typename T>
 hipError_t gemm_patch(const T* A, const T* W, int M, int d, int P, const float* bias, float* z,
                       hipStream_t st);
@@ -71,6 +73,10 @@ hipError_t build_mods_strided(const float* m, const float* e, const float* table
                               long table_stride, int n_blocks, const float* head_table, int d,
                               float* mods, float* hmod, hipStream_t st);
 template <typename T> hipError_t cast_from_f32(const float* src, T* dst, long n, hipStream_t st);
+// z[rows][d] += gate * y (gate: [d] or NULL for 1); d % 8 == 0.  Applies a
+// stored attention-branch output y [rows][d] of the compute type.
+template <typename T>
+hipError_t residual_add(float* z, const T* y, const float* gate, long rows, int d, hipStream_t st);
 
 // ---- cache rule, update, score (k_cache.hip)
 struct DecideOut {     // written by the decision kernel, read back by the host

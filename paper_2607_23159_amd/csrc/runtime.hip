@@ -281,6 +281,11 @@ struct cs_rollout {
   int steps_done = 0;
   int decided_step = 0;
   int n_compute = 0;
+  // attention-output broadcasting (CS_CACHE_PAB): stored branch outputs
+  // [n_blocks][S][L][d] of the compute type, and whether any is stored
+  void *pab_self = nullptr, *pab_cross = nullptr;
+  bool pab_have_self = false, pab_have_cross = false;
+  long long self_reused = 0, cross_reused = 0;
   std::vector<uint8_t> has_ref_h;
   long long calls = 0, computed = 0;
   size_t dec_bytes() const { return sizeof(DecideOut) + (size_t)S * sizeof(double) + (size_t)S; }
@@ -291,7 +296,8 @@ struct cs_rollout {
   ~cs_rollout() {
     ws.release();
     ctx.release();
-    void* ps[] = {x, xref, delta, vbuf, vtil, a, partials, spart, scores, has_ref, ovr, slots, branch, dec};
+    void* ps[] = {x, xref, delta, vbuf, vtil, a, partials, spart, scores, has_ref, ovr, slots, branch, dec,
+                  pab_self, pab_cross};
     for (void* p : ps) if (p) hipFree(p);
     if (dec_host) hipHostFree(dec_host);
     if (ovr_host) hipHostFree(ovr_host);
@@ -384,13 +390,24 @@ static cs_status time_cond(cs_model* m, float t) {
   return CS_OK;
 }
 
+// Attention-output broadcasting for one transformer evaluation: per branch,
+// COMPUTE (no store), STORE (compute and keep the output) or REUSE (apply the
+// kept output).  The arrays are [n_blocks][n_slots][L][d]; rows follow the
+// evaluation's row order, so the slots must be the same streams in the same
+// order on every call of a rollout.
+enum PabMode { PAB_COMPUTE = 0, PAB_STORE = 1, PAB_REUSE = 2 };
+struct PabIO {
+  void* self_y; void* cross_y;
+  int self_mode, cross_mode;
+};
+
 // One transformer evaluation for n_slots streams.  Stream s reads latent
 // x + (slot_id[s] / cand_div) * D, attends to text branch kv_branch[s], and
 // writes its velocity to vout + slot_id[s] * D.
 template <typename T>
 static cs_status dit_forward(cs_model* m, Workspace& w, CtxKV& c, const float* x,
                              const int32_t* slot_id, const int32_t* kv_branch, int n_slots,
-                             int cand_div, float t, float* vout) {
+                             int cand_div, float t, float* vout, const PabIO* pab) {
   const cs_model_desc& g = m->desc;
   hipStream_t st = m->stream;
   Profiler& pf = m->prof;
@@ -413,10 +430,18 @@ static cs_status dit_forward(cs_model* m, Workspace& w, CtxKV& c, const float* x
     HIPC(gemm_patch<T>((const T*)w.patches, (const T*)m->patch_w, (int)rows, (int)d, (int)m->P,
                        m->patch_b, Z, st));
   }
+  const int self_mode = pab ? pab->self_mode : PAB_COMPUTE;
+  const int cross_mode = pab ? pab->cross_mode : PAB_COMPUTE;
   for (int j = 0; j < g.n_blocks; ++j) {
     const Block& bk = m->blocks[j];
     const float* md = m->mods + (long)j * 6 * d;
+    T* y_self = pab ? (T*)pab->self_y + (long)j * rows * d : nullptr;
+    T* y_cross = pab ? (T*)pab->cross_y + (long)j * rows * d : nullptr;
     // self-attention
+    if (self_mode == PAB_REUSE) {
+      ProfScope ps(pf, CS_K_OTHER, st);
+      HIPC(residual_add<T>(Z, y_self, md + 2 * d, rows, (int)d, st));
+    } else {
     { ProfScope ps(pf, CS_K_NORM, st);
       HIPC(layer_norm_mod<T>(Z, rows, (int)d, md + 0 * d, md + 1 * d, 0, U, st)); }
     { ProfScope ps(pf, CS_K_GEMM, st);
@@ -436,8 +461,14 @@ static cs_status dit_forward(cs_model* m, Workspace& w, CtxKV& c, const float* x
       HIPC(flash_attention<T>(a, g.head_dim, st));
     }
     { ProfScope ps(pf, CS_K_GEMM, st);
-      HIPC(gemm_residual<T>(O, d, (const T*)bk.o_w, (int)rows, (int)d, (int)d, bk.o_b, md + 2 * d, Z, st)); }
+      HIPC(gemm_residual<T>(O, d, (const T*)bk.o_w, (int)rows, (int)d, (int)d, bk.o_b, md + 2 * d, Z,
+                            self_mode == PAB_STORE ? y_self : nullptr, st)); }
+    }
     // cross-attention
+    if (cross_mode == PAB_REUSE) {
+      ProfScope ps(pf, CS_K_OTHER, st);
+      HIPC(residual_add<T>(Z, y_cross, nullptr, rows, (int)d, st));
+    } else {
     { ProfScope ps(pf, CS_K_NORM, st);
       HIPC(layer_norm_mod<T>(Z, rows, (int)d, bk.ca_ln_g, bk.ca_ln_b, 1, U, st)); }
     { ProfScope ps(pf, CS_K_GEMM, st);
@@ -456,13 +487,16 @@ static cs_status dit_forward(cs_model* m, Workspace& w, CtxKV& c, const float* x
       HIPC(flash_attention<T>(a, g.head_dim, st));
     }
     { ProfScope ps(pf, CS_K_GEMM, st);
-      HIPC(gemm_residual<T>(O, d, (const T*)bk.cao_w, (int)rows, (int)d, (int)d, bk.cao_b, nullptr, Z, st)); }
+      HIPC(gemm_residual<T>(O, d, (const T*)bk.cao_w, (int)rows, (int)d, (int)d, bk.cao_b, nullptr, Z,
+                            cross_mode == PAB_STORE ? y_cross : nullptr, st)); }
+    }
     // feed-forward
     { ProfScope ps(pf, CS_K_NORM, st);
       HIPC(layer_norm_mod<T>(Z, rows, (int)d, md + 3 * d, md + 4 * d, 0, U, st)); }
     { ProfScope ps(pf, CS_K_GEMM, st);
       HIPC(gemm_store<T>(U, d, (const T*)bk.ffn1_w, (int)rows, F, (int)d, bk.ffn1_b, 1, Hh, F, st));
-      HIPC(gemm_residual<T>(Hh, F, (const T*)bk.ffn2_w, (int)rows, (int)d, F, bk.ffn2_b, md + 5 * d, Z, st)); }
+      HIPC(gemm_residual<T>(Hh, F, (const T*)bk.ffn2_w, (int)rows, (int)d, F, bk.ffn2_b, md + 5 * d, Z,
+                            nullptr, st)); }
   }
   { ProfScope ps(pf, CS_K_NORM, st);
     HIPC(layer_norm_mod<T>(Z, rows, (int)d, m->hmod, m->hmod + d, 0, U, st)); }
@@ -474,10 +508,10 @@ static cs_status dit_forward(cs_model* m, Workspace& w, CtxKV& c, const float* x
 
 static cs_status dit_dispatch(cs_model* m, Workspace& w, CtxKV& c, const float* x,
                               const int32_t* slot_id, const int32_t* kv_branch, int n_slots,
-                              int cand_div, float t, float* vout) {
+                              int cand_div, float t, float* vout, const PabIO* pab = nullptr) {
   if (m->desc.dtype == CS_BF16)
-    return dit_forward<bf16>(m, w, c, x, slot_id, kv_branch, n_slots, cand_div, t, vout);
-  return dit_forward<float>(m, w, c, x, slot_id, kv_branch, n_slots, cand_div, t, vout);
+    return dit_forward<bf16>(m, w, c, x, slot_id, kv_branch, n_slots, cand_div, t, vout, pab);
+  return dit_forward<float>(m, w, c, x, slot_id, kv_branch, n_slots, cand_div, t, vout, pab);
 }
 
 static cs_status ctx_dispatch(cs_model* m, CtxKV& c, int b, const float* ctx) {
@@ -659,8 +693,11 @@ static cs_status validate_rollout(const cs_model* m, const cs_rollout_desc* r) {
   CHECK(r->n_steps >= 1 && r->n_steps <= 100000, CS_E_INVAL, "n_steps must be >= 1");
   CHECK(r->n_branch == 1 || r->n_branch == 2, CS_E_INVAL, "n_branch must be 1 or 2");
   CHECK(r->k_warm >= 0 && r->k_cool >= 0, CS_E_INVAL, "k_warm and k_cool must be >= 0");
-  CHECK(r->mode == CS_CACHE_OFF || r->mode == CS_CACHE_ADAPTIVE || r->mode == CS_CACHE_STATIC,
+  CHECK(r->mode == CS_CACHE_OFF || r->mode == CS_CACHE_ADAPTIVE || r->mode == CS_CACHE_STATIC ||
+            r->mode == CS_CACHE_PAB,
         CS_E_INVAL, "unknown cache mode %d", r->mode);
+  CHECK(r->mode != CS_CACHE_PAB || (r->pab_self_range >= 1 && r->pab_cross_range >= 1), CS_E_INVAL,
+        "pab_self_range and pab_cross_range must be >= 1");
   CHECK(!(r->tau != r->tau) && r->tau >= 0.0f, CS_E_INVAL, "tau must be >= 0 and not NaN");
   CHECK(isfinite(r->guidance), CS_E_INVAL, "guidance must be finite");
   CHECK(r->mode != CS_CACHE_STATIC || r->static_k >= 1, CS_E_INVAL, "static_k must be >= 1");
@@ -710,6 +747,11 @@ static cs_status rollout_init_impl(cs_model* m, const cs_rollout_desc* desc, con
   HIPC(hipHostMalloc((void**)&r->scores_host, N * sizeof(double), hipHostMallocDefault));
   TRY(ws_alloc(m, r->ws, (int)S));
   TRY(ctx_alloc(m, r->ctx, desc->n_branch));
+  if (desc->mode == CS_CACHE_PAB) {
+    const size_t bytes = (size_t)m->desc.n_blocks * S * m->L * m->d * m->esz;
+    TRY(dmalloc(&r->pab_self, bytes));
+    TRY(dmalloc(&r->pab_cross, bytes));
+  }
   // reset cache state (Alg. 1: reset at the start of every generation)
   HIPC(hipMemcpyAsync(r->x, x1, N * D * sizeof(float), hipMemcpyDeviceToDevice, st));
   HIPC(hipMemsetAsync(r->xref, 0, S * D * sizeof(float), st));
@@ -741,6 +783,8 @@ static cs_status decide_impl(cs_rollout* r, int32_t step, const uint8_t* ovr, ui
   CHECK(step >= 1 && step <= r->desc.n_steps, CS_E_INVAL, "step %d outside 1..%d", step, r->desc.n_steps);
   CHECK(step == r->steps_done + 1, CS_E_STATE, "step %d requested, next step is %d", step, r->steps_done + 1);
   CHECK(r->decided_step != step, CS_E_STATE, "step %d already decided", step);
+  CHECK(!(ovr && r->desc.mode == CS_CACHE_PAB), CS_E_UNSUPPORTED,
+        "a replay override is not available in CS_CACHE_PAB mode");
   cs_model* m = r->model;
   hipStream_t st = m->stream;
   const cs_rollout_desc& d = r->desc;
@@ -790,15 +834,30 @@ static cs_status step_impl(cs_rollout* r, int32_t step) {
   const cs_rollout_desc& d = r->desc;
   // the decision kernel left the computed streams (and their text branch)
   // compacted on the device; only their count was read back
-  if (r->n_compute > 0) {
+  if (d.mode == CS_CACHE_PAB) {
+    // every call computes (the decision compacted all S streams in order);
+    // the attention branches follow the broadcast schedule
+    CHECK(r->n_compute == r->S, CS_E_STATE, "PAB step %d: %d of %d calls computing", step,
+          r->n_compute, r->S);
+    const bool window = step <= d.k_warm || step > d.n_steps - d.k_cool;
+    const bool cs_ = window || !r->pab_have_self || (step - d.k_warm) % d.pab_self_range == 0;
+    const bool cc_ = window || !r->pab_have_cross || (step - d.k_warm) % d.pab_cross_range == 0;
+    PabIO io{r->pab_self, r->pab_cross, cs_ ? PAB_STORE : PAB_REUSE, cc_ ? PAB_STORE : PAB_REUSE};
+    TRY(dit_dispatch(m, r->ws, r->ctx, r->x, r->slots, r->branch, r->n_compute, d.n_branch,
+                     r->t[step - 1], r->vbuf, &io));
+    r->pab_have_self = r->pab_have_cross = true;
+    if (!cs_) r->self_reused += r->S;
+    if (!cc_) r->cross_reused += r->S;
+  } else if (r->n_compute > 0) {
     TRY(dit_dispatch(m, r->ws, r->ctx, r->x, r->slots, r->branch, r->n_compute, d.n_branch,
                      r->t[step - 1], r->vbuf));
   }
   {
     ProfScope ps(m->prof, CS_K_UPDATE, st);
     const float dt = r->t[step] - r->t[step - 1];
+    const int store_state = d.mode == CS_CACHE_ADAPTIVE || d.mode == CS_CACHE_STATIC;
     HIPC(cache_update(r->x, r->xref, r->delta, r->vbuf, r->mask_dev(), d.n_cand, d.n_branch, r->D, dt,
-                      d.guidance, d.mode != CS_CACHE_OFF ? 1 : 0, r->vtil, st));
+                      d.guidance, store_state, r->vtil, st));
     if (r->vtil) r->vtil_step = step;
   }
   r->calls += r->S;
@@ -867,6 +926,7 @@ cs_status cs_preview_score(cs_rollout* r, const float* w, double* scores) {
 cs_status cs_rollout_retain(cs_rollout* r, const int32_t* keep, int32_t n_keep) {
   GUARD({
     CHECK(r && keep, CS_E_INVAL, "rollout and keep must be non-NULL");
+    CHECK(r->desc.mode != CS_CACHE_PAB, CS_E_UNSUPPORTED, "retain is not available in CS_CACHE_PAB mode");
     const int N = r->desc.n_cand, B = r->desc.n_branch;
     CHECK(n_keep >= 1 && n_keep <= N, CS_E_INVAL, "n_keep must be in [1, %d]", N);
     for (int j = 0; j < n_keep; ++j) {
@@ -918,6 +978,8 @@ cs_status cs_rollout_stats(cs_rollout* r, cs_rollout_stats_t* out) {
     out->steps_done = r->steps_done;
     out->calls = r->calls;
     out->computed = r->computed;
+    out->self_reused = r->self_reused;
+    out->cross_reused = r->cross_reused;
     return CS_OK;
   })
 }
@@ -929,6 +991,7 @@ static const uint64_t CKPT_MAGIC = 0x43535f524f4c4c31ull;  // "CS_ROLL1"
 cs_status cs_rollout_export(cs_rollout* r, void* buf, size_t* bytes) {
   GUARD({
     CHECK(r && bytes, CS_E_INVAL, "rollout and bytes must be non-NULL");
+    CHECK(r->desc.mode != CS_CACHE_PAB, CS_E_UNSUPPORTED, "checkpoints are not available in CS_CACHE_PAB mode");
     const size_t N = r->desc.n_cand, S = r->S, D = r->D;
     const size_t need = sizeof(CkptHeader) + (N * D + 2 * S * D) * sizeof(float) + S * sizeof(double) + S;
     if (!buf) { *bytes = need; return CS_OK; }
@@ -954,6 +1017,7 @@ cs_status cs_rollout_export(cs_rollout* r, void* buf, size_t* bytes) {
 cs_status cs_rollout_import(cs_rollout* r, const void* buf, size_t bytes) {
   GUARD({
     CHECK(r && buf, CS_E_INVAL, "rollout and buf must be non-NULL");
+    CHECK(r->desc.mode != CS_CACHE_PAB, CS_E_UNSUPPORTED, "checkpoints are not available in CS_CACHE_PAB mode");
     const size_t N = r->desc.n_cand, S = r->S, D = r->D;
     const size_t need = sizeof(CkptHeader) + (N * D + 2 * S * D) * sizeof(float) + S * sizeof(double) + S;
     CHECK(bytes == need, CS_E_INVAL, "checkpoint has %zu bytes, %zu expected", bytes, need);

@@ -63,6 +63,8 @@ class GpuRollout:
     scores: Optional[np.ndarray]   # [N] float64
     computed: int
     calls: int
+    self_reused: int = 0           # PAB: calls that reused stored attention outputs
+    cross_reused: int = 0
 
     def schedule(self, i: int, b: int, n_branch: int) -> List[bool]:
         return [bool(m) for m in self.masks[:, i * n_branch + b]]
@@ -80,7 +82,8 @@ class Inputs:
 def run_rollout(model: GpuModel, wl: Workload, inputs: Optional[Inputs] = None, *,
                 tau: Optional[float] = None, mode: Optional[int] = None,
                 n_cand: Optional[int] = None, override: Optional[np.ndarray] = None,
-                record: bool = True, score: bool = True) -> GpuRollout:
+                record: bool = True, score: bool = True, pab_self: Optional[int] = None,
+                pab_cross: Optional[int] = None) -> GpuRollout:
     """One batched rollout of the first ``n_cand`` seeds of the workload.
 
     ``override`` [T][S] replays a given schedule (1 = compute)."""
@@ -92,6 +95,10 @@ def run_rollout(model: GpuModel, wl: Workload, inputs: Optional[Inputs] = None, 
         kw["tau"] = tau
     if mode is not None:
         kw["mode"] = mode
+    if pab_self is not None:
+        kw["pab_self"] = pab_self
+    if pab_cross is not None:
+        kw["pab_cross"] = pab_cross
     desc = B.RolloutDesc(r, wl.timesteps, **kw)
     S = n * r.n_branch
     x1 = inp.x1[:n]
@@ -112,7 +119,7 @@ def run_rollout(model: GpuModel, wl: Workload, inputs: Optional[Inputs] = None, 
         st = B.cs_rollout_stats(h)
         torch.cuda.synchronize()
         return GpuRollout(lat.cpu().numpy().reshape((n,) + wl.noise.shape[1:]), masks, avals, scores,
-                          int(st.computed), int(st.calls))
+                          int(st.computed), int(st.calls), int(st.self_reused), int(st.cross_reused))
     finally:
         B.cs_rollout_free(h)
 
