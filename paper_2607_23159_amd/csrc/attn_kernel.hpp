@@ -275,4 +275,241 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash(AttnArgs<T> a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 variant with direct global->LDS tile loads.
+//
+// K and V^T tiles of KVT keys travel from global memory straight into a ring
+// of STAGES LDS buffers (no staging registers, no LDS store instructions);
+// tile t+STAGES-1 is requested while tile t is processed, and one barrier per
+// tile separates the reads of a buffer from its refill.  Rows are unpadded;
+// 16-byte chunks are XOR-swizzled so that the fragment reads are free of bank
+// conflicts.
+//
+// V^T is stored in natural key order.  The key order of P^T in the
+// accumulators is made to match it instead: the score product reads, for its
+// output row u, K row pi(u), where pi swaps bits 2 and 3 of u.  Accumulator
+// register j of lane l holds output row u = 8(j/4) + 4(l/32) + j%4, so it
+// holds key pi(u) = 16(j/8) + 8(l/32) + j%8, which is exactly element j%8 of
+// k-step j/8 of the value product's B operand for lane l.  The K swizzle is
+// taken in pi-space, f(r) = swz(pi(r)), so the permuted reads stay
+// conflict-free.
+// ---------------------------------------------------------------------------
+CS_DEV int swap_bits23(int u) { return (u & ~12) | ((u & 4) << 1) | ((u & 8) >> 1); }
+
+template <int DH, int QB, int KVT, int NW, int OCC, int STAGES, bool CROSS>
+__global__ __launch_bounds__(64 * NW, OCC) void k_flash_dl(AttnArgs<bf16> a) {
+  typedef Mfma32<bf16> MF;
+  constexpr int KSTEP = MF::KSTEP;             // 16 keys / channels per MFMA step
+  constexpr int CPR_K = DH / 8, RPI_K = 64 / CPR_K;    // K: chunks per row, rows per load
+  constexpr int CPR_V = KVT / 8, RPI_V = 64 / CPR_V;   // V^T
+  constexpr int K_INST = KVT / RPI_K / NW, V_INST = DH / RPI_V / NW;
+  constexpr int PER_TILE = K_INST + V_INST;    // load instructions per wave per tile
+  constexpr int K_ELEMS = KVT * DH, STAGE = 2 * KVT * DH;
+  constexpr int NKT = KVT / 32, NDT = DH / 32, NKS = DH / KSTEP, NPS = 32 / KSTEP;
+  static_assert(K_INST * RPI_K * NW == KVT && V_INST * RPI_V * NW == DH, "tile split");
+  static_assert(STAGES >= 3 && STAGES <= 4, "ring depth");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[STAGES * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  constexpr int QPW = QB * 32;                 // queries per wave
+  const int n_qt = (a.lq + NW * QPW - 1) / (NW * QPW);
+  const int vid = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int qt = vid % n_qt, hs = vid / n_qt;
+  const int head = hs % a.heads, s = hs / a.heads;
+  const int kvs = a.kv_sel ? a.kv_sel[s] : s;
+  const int q0 = qt * (NW * QPW) + wave * QPW;
+
+  const bf16* qb_ = a.q + (long)s * a.q_ss + head * DH;
+  const bf16* kb_ = a.k + (long)kvs * a.k_ss + head * DH;
+  const bf16* vb_ = a.vt + (long)kvs * a.vt_ss + (long)head * DH * a.vt_ld;
+
+  // Q^T fragments (B operand), kept for the whole key loop
+  typename MF::frag qf[QB][NKS];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int row = min(q0 + qb * 32 + l32, a.lq - 1);
+    const bf16* src = qb_ + (long)row * a.q_ld + MF::KPL * half;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      qf[qb][ks] = MF::load(src + ks * KSTEP);
+      asm volatile("" : "+v"(qf[qb][ks]));
+    }
+  }
+
+  // per-lane load sources: lane covers row (lane / CPR) of its instruction's
+  // rows and physical chunk lane % CPR, i.e. logical chunk phys ^ f(row)
+  int k_row[K_INST], k_col[K_INST];
+#pragma unroll
+  for (int i = 0; i < K_INST; ++i) {
+    const int row = (wave * K_INST + i) * RPI_K + lane / CPR_K;
+    k_row[i] = row;
+    k_col[i] = ((lane % CPR_K) ^ chunk_swz<CPR_K>(swap_bits23(row))) * 8;
+  }
+  const bf16* v_src[V_INST];
+#pragma unroll
+  for (int i = 0; i < V_INST; ++i) {
+    const int row = (wave * V_INST + i) * RPI_V + lane / CPR_V;
+    v_src[i] = vb_ + (long)row * a.vt_ld + ((lane % CPR_V) ^ chunk_swz<CPR_V>(row)) * 8;
+  }
+  auto issue = [&](int tile, int st) {
+    const int kv0 = tile * KVT;
+    bf16* sk = smem + st * STAGE;
+    bf16* sv = sk + K_ELEMS;
+#pragma unroll
+    for (int i = 0; i < K_INST; ++i) {
+      const int key = min(kv0 + k_row[i], a.lk - 1);   // rows past lk: clamped, masked later
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(kb_ + (long)key * a.k_ld + k_col[i]),
+                                       (lds_void_t*)(sk + (wave * K_INST + i) * RPI_K * DH), 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < V_INST; ++i)
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(v_src[i] + kv0),
+                                       (lds_void_t*)(sv + (wave * V_INST + i) * RPI_V * KVT), 16, 0, 0);
+  };
+
+  f32x16 o[QB][NDT];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[qb][dt][r] = 0.0f;
+  float m_run[QB], l_run[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.0f; }
+
+  const int ntiles = (a.lk + KVT - 1) / KVT;
+#pragma unroll
+  for (int t = 0; t < STAGES - 1; ++t)
+    if (t < ntiles) issue(t, t);
+
+  // fragment rows: the score product reads K row pi(l32) of each 32-key
+  // block; the value product reads V^T row (channel) l32 of each 32-block
+  const int k_frag_row = swap_bits23(l32);
+
+  for (int t = 0; t < ntiles; ++t) {
+    // tile t has landed once at most min(rem, STAGES-2) later tiles are in flight
+    const int rem = ntiles - 1 - t;
+    if (rem >= STAGES - 2) wait_vm_barrier<(STAGES - 2) * PER_TILE>();
+    else if (STAGES == 4 && rem == 1) wait_vm_barrier<PER_TILE>();
+    else wait_vm_barrier<0>();
+    if (t + STAGES - 1 < ntiles) issue(t + STAGES - 1, (t + STAGES - 1) % STAGES);
+    const bf16* sk = smem + (t % STAGES) * STAGE;
+    const bf16* sv = sk + K_ELEMS;
+    const int kv0 = t * KVT;
+
+    // S^T = K Q^T (rows in pi order)
+    f32x16 sc[NKT][QB];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[kt][qb][r] = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        const int row = kt * 32 + k_frag_row;
+        const int c = 2 * ks + half;
+        typename MF::frag kf = MF::load(sk + row * DH + (c ^ chunk_swz<CPR_K>(kt * 32 + l32)) * 8);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) sc[kt][qb] = MF::mma(kf, qf[qb][ks], sc[kt][qb]);
+      }
+    }
+    if (kv0 + KVT > a.lk) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kv0 + kt * 32 + swap_bits23(acc_row(r, lane));
+          if (key >= a.lk)
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) sc[kt][qb][r] = -INFINITY;
+        }
+    }
+
+    // online softmax with lazy rescaling (see k_flash); P^T packed into
+    // B-operand fragments, row sums over the rounded operands
+    typename MF::frag pf[QB][NKT][NPS];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][qb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * a.scale_log2;
+      if (__any(mx > m_run[qb] + RESCALE_LOG2)) {
+        const float m_new = fmaxf(m_run[qb], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[qb][dt][r] *= alpha;
+      }
+      float lsum = 0.0f;
+      const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        float p[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          p[r] = __builtin_amdgcn_exp2f(fmaf(sc[kt][qb][r], a.scale_log2, -m_run[qb]));
+#pragma unroll
+        for (int ps = 0; ps < NPS; ++ps) {
+          typename MF::frag f;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) f[i] = (bf16)p[ps * 8 + i];
+          pf[qb][kt][ps] = f;
+#pragma unroll
+          for (int i = 0; i < 8; i += 2) {
+            const bf16x2 pr = {f[i], f[i + 1]};
+            lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, one, lsum, false);
+          }
+        }
+      }
+      l_run[qb] += lsum;
+    }
+
+    // O^T += V^T P^T
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int ps = 0; ps < NPS; ++ps)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const int row = dt * 32 + l32;
+          const int c = 4 * kt + 2 * ps + half;
+          typename MF::frag vf = MF::load(sv + row * KVT + (c ^ chunk_swz<CPR_V>(row)) * 8);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) o[qb][dt] = MF::mma(vf, pf[qb][kt][ps], o[qb][dt]);
+        }
+  }
+
+  // normalise and store O[q][head*DH + channel]
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32, WAVE);
+    const float inv = 1.0f / l_tot;
+    const int row = q0 + qb * 32 + l32;
+    if (row < a.lq) {
+      bf16* dst = a.o + (long)s * a.o_ss + (long)row * a.o_ld + head * DH;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int ch = dt * 32 + 8 * g + 4 * half;
+          bf16x4 q;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) q[r] = (bf16)(o[qb][dt][4 * g + r] * inv);
+          *reinterpret_cast<bf16x4*>(dst + ch) = q;
+        }
+    }
+  }
+}
+
 }  // namespace cs

@@ -91,5 +91,27 @@ CS_DEV int xcd_contiguous(int bid, int nwg) {
   return x * per + min(x, rem) + (bid >> 3);
 }
 
+// ---- direct global->LDS loads (gfx950 global_load_lds_dwordx4): each
+// wave instruction moves 64 x 16 bytes into 1 KB of LDS at base + 16*lane,
+// with an arbitrary global address per lane.
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
+
+// XOR swizzle of the 16-byte chunks of LDS rows that hold CPR chunks each:
+// chunk c of row r is stored at c ^ chunk_swz(r), so that 16-byte reads of
+// one logical chunk from 16 (or 8) consecutive rows hit distinct banks.
+template <int CPR> CS_DEV int chunk_swz(int r) {
+  static_assert(CPR == 2 || CPR == 4 || CPR == 8 || CPR == 16, "chunks per row");
+  constexpr int LOG = CPR == 2 ? 1 : (CPR == 4 ? 2 : (CPR == 8 ? 3 : 4));
+  return (r ^ (r >> LOG)) & (CPR - 1);
+}
+
+// Wait until at most n vector-memory operations of this wave are
+// outstanding, then barrier; the memory clobber keeps the compiler from moving
+// LDS accesses across it.
+template <int n> CS_DEV void wait_vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(n) : "memory");
+}
+
 inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 inline long round_up(long a, long b) { return (a + b - 1) / b * b; }

@@ -251,21 +251,6 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
 // row r is stored at chunk c ^ f(r), f(r) = (r ^ (r >> log2 CPR)) & (CPR-1),
 // which keeps the 32-row fragment reads free of bank conflicts.
 // ---------------------------------------------------------------------------
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void gbl_void_t;
-
-template <int CPR> CS_DEV int chunk_swz(int r) {
-  constexpr int LOG = CPR == 4 ? 2 : (CPR == 8 ? 3 : 1);
-  return (r ^ (r >> LOG)) & (CPR - 1);
-}
-
-// Wait until at most n vector-memory operations of this wave are
-// outstanding, then barrier; the memory clobber keeps the compiler from moving
-// LDS accesses across it.
-template <int n> CS_DEV void wait_vm_barrier() {
-  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(n) : "memory");
-}
-
 template <int BM, int BN, int BK, int WM, int WN, int NWAVE, int OCC, int STAGES, int GM,
           class Epi>
 __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restrict__ A, long lda,
