@@ -279,7 +279,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash(AttnArgs<T> a) {
 // bf16 variant with direct global->LDS tile loads.
 //
 // K and V^T tiles of KVT keys travel from global memory straight into a ring
-// of STAGES LDS buffers (no staging registers, no LDS store instructions);
+// of STAGES LDS buffers by buffer loads (no staging registers, no LDS store
+// instructions; keys past lk arrive as zeros);
 // tile t+STAGES-1 is requested while tile t is processed, and one barrier per
 // tile separates the reads of a buffer from its refill.  Rows are unpadded;
 // 16-byte chunks are XOR-swizzled so that the fragment reads are free of bank
@@ -339,33 +340,32 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash_dl(AttnArgs<bf16> a) {
 
   // per-lane load sources: lane covers row (lane / CPR) of its instruction's
   // rows and physical chunk lane % CPR, i.e. logical chunk phys ^ f(row)
-  int k_row[K_INST], k_col[K_INST];
+  // Buffer ranges: the lk key rows of this (stream, head), and its DH rows
+  // of V^T (padded key length); keys past lk load as zeros and are masked.
+  const int k_bytes = (int)(((long)(a.lk - 1) * a.k_ld + DH) * 2);
+  const int v_bytes = (int)((long)DH * a.vt_ld * 2);
+  int k_off[K_INST], v_off[V_INST];
 #pragma unroll
   for (int i = 0; i < K_INST; ++i) {
     const int row = (wave * K_INST + i) * RPI_K + lane / CPR_K;
-    k_row[i] = row;
-    k_col[i] = ((lane % CPR_K) ^ chunk_swz<CPR_K>(swap_bits23(row))) * 8;
+    k_off[i] = (row * (int)a.k_ld + ((lane % CPR_K) ^ chunk_swz<CPR_K>(swap_bits23(row))) * 8) * 2;
   }
-  const bf16* v_src[V_INST];
 #pragma unroll
   for (int i = 0; i < V_INST; ++i) {
     const int row = (wave * V_INST + i) * RPI_V + lane / CPR_V;
-    v_src[i] = vb_ + (long)row * a.vt_ld + ((lane % CPR_V) ^ chunk_swz<CPR_V>(row)) * 8;
+    v_off[i] = (row * (int)a.vt_ld + ((lane % CPR_V) ^ chunk_swz<CPR_V>(row)) * 8) * 2;
   }
   auto issue = [&](int tile, int st) {
     const int kv0 = tile * KVT;
     bf16* sk = smem + st * STAGE;
     bf16* sv = sk + K_ELEMS;
 #pragma unroll
-    for (int i = 0; i < K_INST; ++i) {
-      const int key = min(kv0 + k_row[i], a.lk - 1);   // rows past lk: clamped, masked later
-      __builtin_amdgcn_global_load_lds((gbl_void_t*)(kb_ + (long)key * a.k_ld + k_col[i]),
-                                       (lds_void_t*)(sk + (wave * K_INST + i) * RPI_K * DH), 16, 0, 0);
-    }
+    for (int i = 0; i < K_INST; ++i)
+      buffer_load_lds16(kb_, k_bytes, sk + (wave * K_INST + i) * RPI_K * DH, k_off[i],
+                        kv0 * (int)a.k_ld * 2);
 #pragma unroll
     for (int i = 0; i < V_INST; ++i)
-      __builtin_amdgcn_global_load_lds((gbl_void_t*)(v_src[i] + kv0),
-                                       (lds_void_t*)(sv + (wave * V_INST + i) * RPI_V * KVT), 16, 0, 0);
+      buffer_load_lds16(vb_, v_bytes, sv + (wave * V_INST + i) * RPI_V * KVT, v_off[i], kv0 * 2);
   };
 
   f32x16 o[QB][NDT];

@@ -97,6 +97,21 @@ CS_DEV int xcd_contiguous(int bid, int nwg) {
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 
+// The same through the buffer path (buffer_load_dwordx4 ... lds): a raw
+// buffer descriptor over [base, base + bytes) and a 32-bit per-lane byte
+// offset voff plus a wave-uniform byte offset soff.  Lanes whose 16 bytes do
+// not lie inside the range receive zeros without any memory access.  The
+// address unit handles a 32-bit offset per lane instead of a 64-bit address,
+// which measured 3-10% faster in the GEMM main loop.  Kept out of lambdas:
+// the builtins exist for the device pass only.
+__device__ __forceinline__ void buffer_load_lds16(const void* base, int bytes, void* lds, int voff,
+                                                  int soff) {
+  // dword 3 of the descriptor: 32-bit data format, no swizzle, raw access
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes,
+                                                                     0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 16, voff, soff, 0, 0);
+}
+
 // XOR swizzle of the 16-byte chunks of LDS rows that hold CPR chunks each:
 // chunk c of row r is stored at c ^ chunk_swz(r), so that 16-byte reads of
 // one logical chunk from 16 (or 8) consecutive rows hit distinct banks.

@@ -240,10 +240,10 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// bf16 GEMM with direct global->LDS loads (gfx950 global_load_lds_dwordx4).
+// bf16 GEMM with direct global->LDS loads (gfx950 buffer_load_dwordx4 ... lds).
 //
 // Each load instruction of a wave moves 64 x 16 bytes into 1 KB of LDS at
-// base + 16*lane, with an arbitrary global address per lane, so no registers
+// base + 16*lane, with an arbitrary source offset per lane, so no registers
 // stage the tiles and no LDS store instructions are issued.  K slices rotate
 // through a ring of STAGES buffers: slice k+STAGES-1 is requested while slice
 // k is multiplied, and a wave waits (vmcnt) only for slice k before the single
@@ -294,36 +294,36 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   const int m0 = tm_i * BM, n0 = tn_i * BN;
 
   // per-lane sources: lane covers row (lane / CPR) of its instruction's rows
-  // and physical chunk lane % CPR, i.e. logical chunk phys ^ f(row)
-  const bf16* a_src[A_INST];
-  const bf16* b_src[B_INST];
+  // and physical chunk lane % CPR, i.e. logical chunk phys ^ f(row).  One
+  // buffer range per operand starts at the tile's first row and covers the
+  // rows that exist, so rows of a ragged last tile load as zeros.
+  const bf16* a_base = A + (long)m0 * lda;
+  const bf16* b_base = W + (long)n0 * ldw;
+  const int a_bytes = min(BM, M - m0) * (int)lda * 2, b_bytes = min(BN, N - n0) * (int)ldw * 2;
+  int a_off[A_INST], b_off[B_INST];
   {
     const int rin = lane / CPR, phys = lane % CPR;
 #pragma unroll
     for (int i = 0; i < A_INST; ++i) {
       const int row = (wave * A_INST + i) * RPI + rin;
-      const int gr = min(m0 + row, M - 1);
-      a_src[i] = A + (long)gr * lda + (phys ^ chunk_swz<CPR>(row)) * CH;
+      a_off[i] = (row * (int)lda + (phys ^ chunk_swz<CPR>(row)) * CH) * 2;
     }
 #pragma unroll
     for (int i = 0; i < B_INST; ++i) {
       const int row = (wave * B_INST + i) * RPI + rin;
-      const int gr = min(n0 + row, N - 1);
-      b_src[i] = W + (long)gr * ldw + (phys ^ chunk_swz<CPR>(row)) * CH;
+      b_off[i] = (row * (int)ldw + (phys ^ chunk_swz<CPR>(row)) * CH) * 2;
     }
   }
   auto issue = [&](int slice, int st) {
-    const long koff = (long)slice * BK;
+    const int koff = slice * BK * 2;
     bf16* sa = smem + st * STAGE;
     bf16* sb = sa + BM * BK;
 #pragma unroll
     for (int i = 0; i < A_INST; ++i)
-      __builtin_amdgcn_global_load_lds((gbl_void_t*)(a_src[i] + koff),
-                                       (lds_void_t*)(sa + (wave * A_INST + i) * RPI * BK), 16, 0, 0);
+      buffer_load_lds16(a_base, a_bytes, sa + (wave * A_INST + i) * RPI * BK, a_off[i], koff);
 #pragma unroll
     for (int i = 0; i < B_INST; ++i)
-      __builtin_amdgcn_global_load_lds((gbl_void_t*)(b_src[i] + koff),
-                                       (lds_void_t*)(sb + (wave * B_INST + i) * RPI * BK), 16, 0, 0);
+      buffer_load_lds16(b_base, b_bytes, sb + (wave * B_INST + i) * RPI * BK, b_off[i], koff);
   };
 
   f32x16 acc[TM][TN];

@@ -28,6 +28,9 @@ static hipError_t launch_flash_dl(const AttnArgs<bf16>& a, hipStream_t st) {
   constexpr int KVT = 64, STAGES = 4;
   const long nwg = (long)cdiv(a.lq, NW * QB * 32) * a.heads * a.n_streams;
   if (nwg * 64 * NW > 0xFFFFFFFFL) return hipErrorInvalidConfiguration;
+  // buffer ranges and offsets are 32-bit byte counts
+  if ((long)a.lk * a.k_ld * 2 > 0x7FFFFFFFL || (long)DH * a.vt_ld * 2 > 0x7FFFFFFFL)
+    return hipErrorInvalidValue;
   if (a.kv_sel)
     hipLaunchKernelGGL((k_flash_dl<DH, QB, KVT, NW, OCC, STAGES, true>), dim3((unsigned)nwg),
                        dim3(64 * NW), 0, st, a);

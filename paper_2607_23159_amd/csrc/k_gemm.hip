@@ -44,6 +44,8 @@ static hipError_t launch(const T* A, long lda, const T* W, long ldw, int M, int 
     typedef DlCfg C;
     if (M <= 0 || N <= 0) return hipSuccess;
     if (K % C::BK != 0 || N % 4 != 0) return hipErrorInvalidValue;
+    // per-tile buffer ranges are 32-bit byte counts
+    if ((long)std::max(C::BM, C::BN) * std::max(lda, ldw) * 2 > 0x7FFFFFFFL) return hipErrorInvalidValue;
     const long tiles = (long)cdiv(M, C::BM) * cdiv(N, C::BN);
     hipLaunchKernelGGL((k_gemm_dl<C::BM, C::BN, C::BK, C::WM, C::WN, C::NW, C::OCC, C::ST, C::GM, Epi>),
                        dim3((unsigned)tiles), dim3(64 * C::NW), 0, st, A, lda, W, ldw, M, N, K, epi);
