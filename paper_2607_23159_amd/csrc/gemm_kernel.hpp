@@ -270,6 +270,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   static_assert(A_INST * RPI * NWAVE == BM && B_INST * RPI * NWAVE == BN, "load split");
   static_assert((BM / WM) * WAVES_N == NWAVE, "wave grid");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+  static_assert(BN * BK * 2 == 32768 && RPI * BK * 2 == 1024, "tiled W block layout");
   __shared__ __attribute__((aligned(1024))) bf16 smem[STAGES * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -297,9 +298,14 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   // and physical chunk lane % CPR, i.e. logical chunk phys ^ f(row).  One
   // buffer range per operand starts at the tile's first row and covers the
   // rows that exist, so rows of a ragged last tile load as zeros.
+  //
+  // W is stored pre-tiled (gemm_tile_weight): the BN x BK block of tile-column
+  // tn and slice kt is 32 KB contiguous at ((tn * nk + kt) * BN * BK)
+  // elements, already in this kernel's LDS layout, so each load instruction
+  // copies 1 KB contiguous.
   const bf16* a_base = A + (long)m0 * lda;
-  const bf16* b_base = W + (long)n0 * ldw;
-  const int a_bytes = min(BM, M - m0) * (int)lda * 2, b_bytes = min(BN, N - n0) * (int)ldw * 2;
+  const bf16* b_base = W + (long)tn_i * BN * K;
+  const int a_bytes = min(BM, M - m0) * (int)lda * 2, b_bytes = BN * K * 2;
   int a_off[A_INST], b_off[B_INST];
   {
     const int rin = lane / CPR, phys = lane % CPR;
@@ -309,21 +315,18 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
       a_off[i] = (row * (int)lda + (phys ^ chunk_swz<CPR>(row)) * CH) * 2;
     }
 #pragma unroll
-    for (int i = 0; i < B_INST; ++i) {
-      const int row = (wave * B_INST + i) * RPI + rin;
-      b_off[i] = (row * (int)ldw + (phys ^ chunk_swz<CPR>(row)) * CH) * 2;
-    }
+    for (int i = 0; i < B_INST; ++i) b_off[i] = (wave * B_INST + i) * 1024 + lane * 16;
   }
   auto issue = [&](int slice, int st) {
-    const int koff = slice * BK * 2;
     bf16* sa = smem + st * STAGE;
     bf16* sb = sa + BM * BK;
 #pragma unroll
     for (int i = 0; i < A_INST; ++i)
-      buffer_load_lds16(a_base, a_bytes, sa + (wave * A_INST + i) * RPI * BK, a_off[i], koff);
+      buffer_load_lds16(a_base, a_bytes, sa + (wave * A_INST + i) * RPI * BK, a_off[i], slice * BK * 2);
 #pragma unroll
     for (int i = 0; i < B_INST; ++i)
-      buffer_load_lds16(b_base, b_bytes, sb + (wave * B_INST + i) * RPI * BK, b_off[i], koff);
+      buffer_load_lds16(b_base, b_bytes, sb + (wave * B_INST + i) * RPI * BK, b_off[i],
+                        slice * BN * BK * 2);
   };
 
   f32x16 acc[TM][TN];

@@ -26,6 +26,40 @@ struct DlCfg {
                        GM = 4;
 };
 
+// ------------------------------------------------------- weight tiling
+// bf16 weights for the direct-load kernel: [N][K] fp32 row-major ->
+// blocks of DlCfg::BN rows x DlCfg::BK columns, block (tn, kt) at
+// ((tn * K/BK + kt) * BN * BK) elements; inside a block row r holds its 8
+// chunks of 8 columns with logical chunk c at physical position
+// c ^ chunk_swz(r), the LDS layout of the kernel.  Rows past N are zero.
+__global__ __launch_bounds__(256) void k_tile_weight(const float* __restrict__ src, int N, int K,
+                                                     bf16* __restrict__ dst, long n_chunks) {
+  constexpr int BN = DlCfg::BN, BK = DlCfg::BK, CPR = BK / 8;
+  const long q = (long)blockIdx.x * 256 + threadIdx.x;
+  if (q >= n_chunks) return;
+  const long blk = q / (BN * CPR);
+  const int within = (int)(q - blk * BN * CPR);
+  const int r = within / CPR, p = within % CPR;
+  const int nk = K / BK;
+  const int tn = (int)(blk / nk), kt = (int)(blk % nk);
+  const int n = tn * BN + r;
+  const int k0 = kt * BK + (p ^ chunk_swz<CPR>(r)) * 8;
+  bf16x8 v;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = n < N ? (bf16)src[(long)n * K + k0 + e] : (bf16)0.0f;
+  *reinterpret_cast<bf16x8*>(dst + q * 8) = v;
+}
+
+long gemm_tiled_weight_elems(int N, int K) { return round_up(N, DlCfg::BN) * (long)K; }
+
+hipError_t gemm_tile_weight(const float* src, int N, int K, bf16* dst, hipStream_t st) {
+  if (N <= 0 || K % DlCfg::BK != 0) return hipErrorInvalidValue;
+  const long n_chunks = gemm_tiled_weight_elems(N, K) / 8;
+  hipLaunchKernelGGL(k_tile_weight, dim3((unsigned)cdiv(n_chunks, 256)), dim3(256), 0, st, src, N, K, dst,
+                     n_chunks);
+  return hipGetLastError();
+}
+
 template <typename T, class C, class Epi>
 static hipError_t launch_staged(const T* A, long lda, const T* W, long ldw, int M, int N, int K,
                                 Epi epi, hipStream_t st) {
@@ -44,8 +78,9 @@ static hipError_t launch(const T* A, long lda, const T* W, long ldw, int M, int 
     typedef DlCfg C;
     if (M <= 0 || N <= 0) return hipSuccess;
     if (K % C::BK != 0 || N % 4 != 0) return hipErrorInvalidValue;
-    // per-tile buffer ranges are 32-bit byte counts
-    if ((long)std::max(C::BM, C::BN) * std::max(lda, ldw) * 2 > 0x7FFFFFFFL) return hipErrorInvalidValue;
+    // W is pre-tiled (row stride K); per-tile buffer ranges are 32-bit byte counts
+    if (ldw != K) return hipErrorInvalidValue;
+    if ((long)std::max(C::BM, C::BN) * std::max(lda, (long)K) * 2 > 0x7FFFFFFFL) return hipErrorInvalidValue;
     const long tiles = (long)cdiv(M, C::BM) * cdiv(N, C::BN);
     hipLaunchKernelGGL((k_gemm_dl<C::BM, C::BN, C::BK, C::WM, C::WN, C::NW, C::OCC, C::ST, C::GM, Epi>),
                        dim3((unsigned)tiles), dim3(64 * C::NW), 0, st, A, lda, W, ldw, M, N, K, epi);

@@ -5,8 +5,11 @@
 
 namespace cs {
 
-// ---- GEMM (k_gemm.hip).  W is [N][K] row-major (K contiguous); every
-// variant adds a bias vector (non-NULL) in its epilogue.
+// ---- GEMM (k_gemm.hip).  W is [N][K] (K contiguous); every variant adds a
+// bias vector (non-NULL) in its epilogue.  bf16 weights are stored in the
+// tiled layout of gemm_tile_weight, fp32 weights row-major.
+long gemm_tiled_weight_elems(int N, int K);
+hipError_t gemm_tile_weight(const float* src, int N, int K, bf16* dst, hipStream_t st);
 template <typename T>
 hipError_t gemm_store(const T* A, long lda, const T* W, int M, int N, int K, const float* bias,
                       int act, T* out, long ldo, hipStream_t st);

@@ -562,7 +562,13 @@ static cs_status model_init_impl(const cs_model_desc* desc, const float* weights
   m->Ltp = round_up(desc->text_len, kvt);
 
   // arena: matrices in the compute type, vectors fp32; block modulation
-  // tables gathered into one [n_blocks][6][d] array.
+  // tables gathered into one [n_blocks][6][d] array.  In bf16 the weights of
+  // the direct-load GEMM (every matrix except the three time-conditioning
+  // GEMV matrices and the narrow head) are stored in its tiled layout.
+  auto tiled = [&](const TSpec& t) {
+    return m->esz == 2 && t.matrix && t.name != "time1_w" && t.name != "time2_w" &&
+           t.name != "mod_w" && t.name != "head_w";
+  };
   std::vector<size_t> off(spec.size());
   size_t bytes = 0;
   const size_t tables_bytes = (size_t)desc->n_blocks * 6 * m->d * sizeof(float);
@@ -572,7 +578,9 @@ static cs_status model_init_impl(const cs_model_desc* desc, const float* weights
     const bool is_table = spec[i].name.size() > 4 && spec[i].name.compare(spec[i].name.size() - 4, 4, ".mod") == 0;
     if (is_table) { off[i] = (size_t)-1; continue; }
     off[i] = bytes;
-    bytes += round_up((size_t)(spec[i].rows * spec[i].cols) * (spec[i].matrix ? m->esz : 4), 256);
+    const long elems = tiled(spec[i]) ? gemm_tiled_weight_elems((int)spec[i].rows, (int)spec[i].cols)
+                                      : spec[i].rows * spec[i].cols;
+    bytes += round_up((size_t)elems * (spec[i].matrix ? m->esz : 4), 256);
   }
   TRY(dmalloc(&m->arena, bytes));
   char* base = (char*)m->arena;
@@ -588,7 +596,9 @@ static cs_status model_init_impl(const cs_model_desc* desc, const float* weights
       ptr[i] = dst;
       ++table_j;
     } else if (spec[i].matrix) {
-      if (m->esz == 2)
+      if (tiled(spec[i]))
+        HIPC(gemm_tile_weight(weights + src, (int)spec[i].rows, (int)spec[i].cols, (bf16*)(base + off[i]), st));
+      else if (m->esz == 2)
         HIPC(cast_from_f32<bf16>(weights + src, (bf16*)(base + off[i]), n, st));
       else
         HIPC(hipMemcpyAsync(base + off[i], weights + src, n * sizeof(float), hipMemcpyDeviceToDevice, st));
