@@ -1,0 +1,107 @@
+"""GPU checks at the full Wan2.1-1.3B size in the launch configuration the
+bench times (8 streams of 32,760 tokens in one transformer call).
+
+The oracle cannot run whole full-size rollouts, so they are checked on
+sampled outputs it computes one by one (one block, sampled tokens) and
+through properties that hold at any size: per-stream batch invariance,
+tau = 0 reproducing the uncached rollout bit for bit, tau = inf computing
+only the forced windows, PAB with range 1 reproducing the uncached rollout,
+and a candidate's rollout not depending on which other seeds share its
+batch."""
+import dataclasses
+import math
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from oracle import dit as odit
+from paper_2607_23159_amd import binding as B
+from paper_2607_23159_amd import synth
+from paper_2607_23159_amd.search import GpuModel, run_rollout
+from parity import TOL, rel_l2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+def test_block_8_streams_full_length_sampled():
+    """One Wan2.1-1.3B block, 8 latents of 32,760 tokens in one call (the
+    bench's row count, 262,080 GEMM rows): sampled tokens of two streams
+    against the oracle, and every stream bitwise equal to its own
+    single-stream call."""
+    say("one block, 8 streams x 32760 tokens, bf16")
+    m = synth.MODELS["wan13b_block1"]
+    w = synth.make_weights(m, init="stress")
+    gm = GpuModel(m, w)
+    W = {k: v.astype(np.float64) for k, v in synth.unflatten(m, w).items()}
+    x = synth.make_noise(m, 8, seed0=900)
+    ctx = synth.make_context(m, 1)
+    xd = torch.from_numpy(x.reshape(8, -1)).cuda()
+    cd = torch.from_numpy(ctx).cuda()
+    v8 = gm.velocity(xd, 0.6, cd)
+    emb = odit.text_embedding(ctx, W)
+    rows = np.array([0, 255, 256, 16384, 32511, 32759])
+    for i in (0, 7):
+        vp = odit.patchify(v8[i].cpu().numpy().reshape(x.shape[1:]), 1, 2, 2)
+        ref = odit.velocity(x[i], 0.6, emb, W, m, last_block_rows=rows)
+        err = rel_l2(vp[rows], ref)
+        say(f"  stream {i} sampled rel_l2={err:.3e}")
+        assert err < TOL[0] / 2
+    for i in (0, 3, 7):
+        one = gm.velocity(xd[i:i + 1].contiguous(), 0.6, cd)
+        assert torch.equal(one[0], v8[i])
+    gm.close()
+
+
+@pytest.fixture(scope="module")
+def full_model():
+    m = synth.MODELS["wan13b"]
+    w = synth.make_weights(m)
+    gm = GpuModel(m, w)
+    yield m, w, gm
+    gm.close()
+
+
+def _short(m, w, n_cand, seed0=100, **kw):
+    roll = synth.RolloutCfg(n_cand=n_cand, n_steps=4, k_warm=1, k_cool=1, **kw)
+    return synth.Workload(name="wan13b_short", model=m, roll=roll, weights=w,
+                          ctx=[synth.make_context(m, synth.CTX_COND_SEED)],
+                          noise=synth.make_noise(m, n_cand, seed0=seed0),
+                          scorer=synth.make_scorer(m), timesteps=synth.timestep_grid(4))
+
+
+def test_full_model_rollout_properties(full_model):
+    """Full 30-block model, 2 seeds, 4 steps."""
+    m, w, gm = full_model
+    wl = _short(m, w, 2)
+    say("full model: tau=0 vs off")
+    a = run_rollout(gm, wl, tau=0.0)
+    b = run_rollout(gm, wl, mode=synth.CACHE_OFF)
+    assert a.computed == a.calls
+    assert np.array_equal(a.latents, b.latents) and np.array_equal(a.scores, b.scores)
+    say("full model: tau=inf forced only")
+    c = run_rollout(gm, wl, tau=math.inf)
+    assert (c.masks.sum(axis=0) == 2).all()
+    say("full model: PAB range 1 vs off")
+    p = run_rollout(gm, wl, mode=synth.CACHE_PAB, pab_self=1, pab_cross=1)
+    assert np.array_equal(p.latents, b.latents)
+    say("full model: seed 101 alone vs in the batch")
+    one = _short(m, w, 1, seed0=101)
+    assert np.array_equal(one.noise[0], wl.noise[1])
+    s = run_rollout(gm, one, tau=0.1)
+    t = run_rollout(gm, wl, tau=0.1)
+    assert np.array_equal(s.masks[:, 0], t.masks[:, 1])
+    assert np.array_equal(s.latents[0], t.latents[1])
