@@ -418,6 +418,19 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash_dl(AttnArgs<bf16> a) {
         for (int qb = 0; qb < QB; ++qb) sc[kt][qb] = MF::mma(kf, qf[qb][ks], sc[kt][qb]);
       }
     }
+    // every V^T fragment of the tile is requested before the softmax, whose
+    // arithmetic then hides the read latency of the value product
+    typename MF::frag vf[NKT][NPS][NDT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int ps = 0; ps < NPS; ++ps)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const int row = dt * 32 + l32;
+          const int c = 4 * kt + 2 * ps + half;
+          vf[kt][ps][dt] = MF::load(sv + row * KVT + (c ^ chunk_swz<CPR_V>(row)) * 8);
+        }
     if (kv0 + KVT > a.lk) {
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
@@ -481,13 +494,9 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash_dl(AttnArgs<bf16> a) {
 #pragma unroll
       for (int ps = 0; ps < NPS; ++ps)
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          const int row = dt * 32 + l32;
-          const int c = 4 * kt + 2 * ps + half;
-          typename MF::frag vf = MF::load(sv + row * KVT + (c ^ chunk_swz<CPR_V>(row)) * 8);
+        for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-          for (int qb = 0; qb < QB; ++qb) o[qb][dt] = MF::mma(vf, pf[qb][kt][ps], o[qb][dt]);
-        }
+          for (int qb = 0; qb < QB; ++qb) o[qb][dt] = MF::mma(vf[kt][ps][dt], pf[qb][kt][ps], o[qb][dt]);
   }
 
   // normalise and store O[q][head*DH + channel]
