@@ -521,4 +521,233 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash_dl(AttnArgs<bf16> a) {
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// bf16 variant with padded LDS rows (head dims 64 and 128).
+//
+// The direct loads place any 16-byte chunk of global memory anywhere in the
+// 1 KB an instruction fills, so the tiles are stored with padded rows instead
+// of a swizzle: a K row of DH/8 chunks takes DH/8 + 1 chunk slots and a V^T
+// row of 8 chunks takes 9.  The extra slot of a row receives a copy of the
+// row's last chunk (same cache line, no extra traffic) and is never read.
+// Row strides of 272 and 144 bytes spread 16 consecutive rows over all 64
+// banks, and since no chunk index is permuted every fragment read of a tile is
+// one base register plus a compile-time offset: the per-read address
+// arithmetic of the swizzled layout disappears from the key loop.  Stage t of
+// the ring holds K (64 x 17 chunks = 17 KB) then V^T (DH x 9 chunks), all
+// whole 1 KB load instructions, spread over the waves (the first few waves
+// issue one more than the others).  Results are bitwise those of k_flash_dl.
+// ---------------------------------------------------------------------------
+template <int DH, int NW, int OCC, int STAGES, bool CROSS>
+__global__ __launch_bounds__(64 * NW, OCC) void k_flash_pad(AttnArgs<bf16> a) {
+  typedef Mfma32<bf16> MF;
+  typedef typename MF::frag frag;
+  constexpr int KVT = 64, KSTEP = MF::KSTEP;
+  constexpr int CK = DH / 8 + 1, CV = KVT / 8 + 1;   // chunk slots per padded row
+  constexpr int KRS = CK * 16, VRS = CV * 16;        // padded row strides (bytes)
+  constexpr int K_INSTR = KVT * CK / 64, V_INSTR = DH * CV / 64;
+  static_assert(K_INSTR * 64 == KVT * CK && V_INSTR * 64 == DH * CV, "whole 1 KB loads");
+  constexpr int KB = K_INSTR * 1024, STAGE = KB + V_INSTR * 1024;
+  constexpr int TOT = K_INSTR + V_INSTR;             // load instructions per tile
+  constexpr int NPW = (TOT + NW - 1) / NW;           // per wave, for the first NBUSY waves
+  constexpr int NBUSY = TOT - (NPW - 1) * NW;        // the others issue NPW - 1
+  constexpr int NKT = KVT / 32, NDT = DH / 32, NKS = DH / KSTEP, NPS = 32 / KSTEP;
+  static_assert(STAGES >= 3 && STAGES <= 4, "ring depth");
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: loads use SGPR ranges
+  const int half = lane >> 5, l32 = lane & 31;
+  const int n_qt = (a.lq + NW * 32 - 1) / (NW * 32);
+  const int vid = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int qt = vid % n_qt, hs = vid / n_qt;
+  const int head = hs % a.heads, s = hs / a.heads;
+  const int kvs = a.kv_sel ? a.kv_sel[s] : s;
+  const int q0 = qt * (NW * 32) + wave * 32;
+
+  const bf16* qb_ = a.q + (long)s * a.q_ss + head * DH;
+  const bf16* kb_ = a.k + (long)kvs * a.k_ss + head * DH;
+  const bf16* vb_ = a.vt + (long)kvs * a.vt_ss + (long)head * DH * a.vt_ld;
+
+  // Q^T fragments (B operand), kept for the whole key loop
+  frag qf[NKS];
+  {
+    const int row = min(q0 + l32, a.lq - 1);
+    const bf16* src = qb_ + (long)row * a.q_ld + MF::KPL * half;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      qf[ks] = MF::load(src + ks * KSTEP);
+      asm volatile("" : "+v"(qf[ks]));
+    }
+  }
+
+  // load instruction i of this wave fills slots [64g, 64g + 64) of the stage,
+  // g = wave + NW*i; slot p of the K part is row p / CK, chunk p % CK (the
+  // padding slot takes the row's last chunk), likewise for V^T.  Keys past
+  // lk load as zeros (K range) or are finite padding (V^T) and are masked.
+  const int k_bytes = (int)(((long)(a.lk - 1) * a.k_ld + DH) * 2);
+  const int v_bytes = (int)((long)DH * a.vt_ld * 2);
+  int voff[NPW];
+#pragma unroll
+  for (int i = 0; i < NPW; ++i) {
+    const int g = wave + NW * i;
+    if (g < K_INSTR) {
+      const int p = g * 64 + lane, row = p / CK, ch = min(p % CK, CK - 2);
+      voff[i] = (row * (int)a.k_ld + ch * 8) * 2;
+    } else {
+      const int p = (g - K_INSTR) * 64 + lane, row = p / CV, ch = min(p % CV, CV - 2);
+      voff[i] = (row * (int)a.vt_ld + ch * 8) * 2;
+    }
+  }
+  const bool busy = wave < NBUSY;
+  auto issue = [&](int tile, int st) {
+    const int kv0 = tile * KVT;
+    char* base = smem + st * STAGE;
+#pragma unroll
+    for (int i = 0; i < NPW; ++i) {
+      const int g = wave + NW * i;
+      if (i < NPW - 1 || busy) {
+        if (g < K_INSTR)
+          buffer_load_lds16(kb_, k_bytes, base + g * 1024, voff[i], kv0 * (int)a.k_ld * 2);
+        else
+          buffer_load_lds16(vb_, v_bytes, base + g * 1024, voff[i], kv0 * 2);
+      }
+    }
+  };
+
+  f32x16 o[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[dt][r] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  const int ntiles = (a.lk + KVT - 1) / KVT;
+#pragma unroll
+  for (int t = 0; t < STAGES - 1; ++t)
+    if (t < ntiles) issue(t, t);
+
+  // fragment bases: the score product reads K row pi(l32) of each 32-key
+  // block (pi swaps bits 2 and 3, see k_flash_dl), the value product V^T row
+  // (channel) l32 of each 32-channel block
+  const int lane_k = swap_bits23(l32) * KRS + half * 16;
+  const int lane_v = KB + l32 * VRS + half * 16;
+  const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+
+  for (int t = 0; t < ntiles; ++t) {
+    // tile t has landed once at most min(rem, STAGES-2) later tiles are in flight
+    const int inflight = min(ntiles - 1 - t, STAGES - 2);
+    if (busy) {
+      if (inflight >= 2) wait_vm_barrier<2 * NPW>();
+      else if (inflight == 1) wait_vm_barrier<NPW>();
+      else wait_vm_barrier<0>();
+    } else {
+      if (inflight >= 2) wait_vm_barrier<2 * (NPW - 1)>();
+      else if (inflight == 1) wait_vm_barrier<NPW - 1>();
+      else wait_vm_barrier<0>();
+    }
+    if (t + STAGES - 1 < ntiles) issue(t + STAGES - 1, (t + STAGES - 1) % STAGES);
+    const char* pk = smem + (t % STAGES) * STAGE + lane_k;
+    const char* pv = smem + (t % STAGES) * STAGE + lane_v;
+    const int kv0 = t * KVT;
+
+    // S^T = K Q^T (rows in pi order)
+    f32x16 sc[NKT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[kt][r] = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        frag kf = MF::load(reinterpret_cast<const bf16*>(pk + kt * 32 * KRS + ks * 32));
+        sc[kt] = MF::mma(kf, qf[ks], sc[kt]);
+      }
+    // every V^T fragment of the tile is requested before the softmax
+    frag vf[NKT][NPS][NDT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int ps = 0; ps < NPS; ++ps)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+          vf[kt][ps][dt] = MF::load(reinterpret_cast<const bf16*>(pv + dt * 32 * VRS + kt * 64 + ps * 32));
+    if (kv0 + KVT > a.lk) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kv0 + kt * 32 + swap_bits23(acc_row(r, lane));
+          if (key >= a.lk) sc[kt][r] = -INFINITY;
+        }
+    }
+
+    // online softmax with lazy rescaling (see k_flash)
+    frag pf[NKT][NPS];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * a.scale_log2;
+    if (__any(mx > m_run + RESCALE_LOG2)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+    }
+    float lsum = 0.0f;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+      float p[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(sc[kt][r], a.scale_log2, -m_run));
+#pragma unroll
+      for (int ps = 0; ps < NPS; ++ps) {
+        frag f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) f[i] = (bf16)p[ps * 8 + i];
+        pf[kt][ps] = f;
+#pragma unroll
+        for (int i = 0; i < 8; i += 2) {
+          const bf16x2 pr = {f[i], f[i + 1]};
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, one, lsum, false);
+        }
+      }
+    }
+    l_run += lsum;
+
+    // O^T += V^T P^T
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int ps = 0; ps < NPS; ++ps)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) o[dt] = MF::mma(vf[kt][ps][dt], pf[kt][ps], o[dt]);
+  }
+
+  // normalise and store O[q][head*DH + channel]
+  const float l_tot = l_run + __shfl_xor(l_run, 32, WAVE);
+  const float inv = 1.0f / l_tot;
+  const int row = q0 + l32;
+  if (row < a.lq) {
+    bf16* dst = a.o + (long)s * a.o_ss + (long)row * a.o_ld + head * DH;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int ch = dt * 32 + 8 * g + 4 * half;
+        bf16x4 q;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) q[r] = (bf16)(o[dt][4 * g + r] * inv);
+        *reinterpret_cast<bf16x4*>(dst + ch) = q;
+      }
+  }
+}
+
 }  // namespace cs

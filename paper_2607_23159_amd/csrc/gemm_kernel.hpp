@@ -35,7 +35,7 @@ struct GemmShape {
   static_assert(A_CH * NT == BM * CPR && B_CH * NT == BN * CPR, "slice split");
 };
 
-// Accumulator layout shared by both kernels: the products are formed as C^T
+// Accumulator layout of the register-staged kernel: the products are formed as C^T
 // tiles (W fragment as the MFMA A operand), so accumulator (i, j) of a lane
 // holds row i*32 + lane%32 of the wave's sub-tile and, in register 4g + r,
 // column j*32 + 8g + 4(lane/32) + r.  Every group of 4 registers is 4
@@ -111,6 +111,64 @@ CS_DEV void gemm_epilogue(const f32x16 (&acc)[TM][TN], int row_base, int col_bas
     gemm_epilogue_impl<false>(acc, row_base, col_base, lane, M, N, epi);
   else
     gemm_epilogue_impl<true>(acc, row_base, col_base, lane, M, N, epi);
+}
+
+// 16x16 accumulators of the bf16 kernel (v_mfma_f32_16x16x32_bf16), also
+// formed as C^T tiles: accumulator (i, j) of a lane holds row i*16 + lane%16
+// of the wave's sub-tile and, in registers 0..3, columns j*16 + 4(lane/16) ..
+// +3, one vector access in the epilogue.
+template <int TM, int TN>
+CS_DEV void init_acc16_bias(f32x4 (&acc)[TM][TN], const float* __restrict__ bias, int col_base,
+                            int lane, int N) {
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int col0 = col_base + j * 16 + 4 * (lane >> 4);
+    float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (col0 < N) b = *reinterpret_cast<const float4*>(bias + col0);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      acc[i][j][0] = b.x;
+      acc[i][j][1] = b.y;
+      acc[i][j][2] = b.z;
+      acc[i][j][3] = b.w;
+    }
+  }
+}
+
+// Epilogue over 16x16 accumulators, one accumulator (4 columns of one row)
+// per step, the next step's epilogue operands fetched ahead.
+template <bool CHECK, int TM, int TN, class Epi>
+CS_DEV void gemm_epilogue16_impl(const f32x4 (&acc)[TM][TN], int row_base, int col_base, int lane,
+                                 int M, int N, const Epi& epi) {
+  constexpr int NQ = TM * TN;
+  typename Epi::Pre pre[2];
+  auto fetch = [&](int q, int slot) {
+    const int i = q / TN, j = q % TN;
+    const int row = row_base + i * 16 + (lane & 15);
+    const int col0 = col_base + j * 16 + 4 * (lane >> 4);
+    if (!CHECK || (row < M && col0 < N)) pre[slot] = epi.pre(row, col0);
+  };
+  fetch(0, 0);
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    if (q + 1 < NQ) fetch(q + 1, (q + 1) & 1);
+    const int i = q / TN, j = q % TN;
+    const int row = row_base + i * 16 + (lane & 15);
+    const int col0 = col_base + j * 16 + 4 * (lane >> 4);
+    if (!CHECK || (row < M && col0 < N)) {
+      const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      epi(row, col0, v, pre[q & 1]);
+    }
+  }
+}
+
+template <int TM, int TN, class Epi>
+CS_DEV void gemm_epilogue16(const f32x4 (&acc)[TM][TN], int row_base, int col_base, int lane, int M,
+                            int N, const Epi& epi) {
+  if (row_base + TM * 16 <= M && col_base + TN * 16 <= N)
+    gemm_epilogue16_impl<false>(acc, row_base, col_base, lane, M, N, epi);
+  else
+    gemm_epilogue16_impl<true>(acc, row_base, col_base, lane, M, N, epi);
 }
 
 // OCC = waves per SIMD the register budget is sized for; GM = tile-rows per
@@ -240,7 +298,8 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// bf16 GEMM with direct global->LDS loads (gfx950 buffer_load_dwordx4 ... lds).
+// bf16 GEMM with direct global->LDS loads (gfx950 buffer_load_dwordx4 ... lds)
+// and 16x16x32 MFMAs.
 //
 // Each load instruction of a wave moves 64 x 16 bytes into 1 KB of LDS at
 // base + 16*lane, with an arbitrary source offset per lane, so no registers
@@ -249,14 +308,19 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
 // k is multiplied, and a wave waits (vmcnt) only for slice k before the single
 // barrier of each iteration.  LDS rows are unpadded; the 16-byte chunk c of
 // row r is stored at chunk c ^ f(r), f(r) = (r ^ (r >> log2 CPR)) & (CPR-1),
-// which keeps the 32-row fragment reads free of bank conflicts.
+// which keeps the fragment reads (16 rows x 4 chunks per instruction) free of
+// bank conflicts.
+//
+// The 16x16x32 product gives bitwise the same sums as two chained 32x32x16
+// steps over the same K order (checked at all projection shapes), and measured
+// 3-6% faster at the Wan2.1-1.3B projection sizes: with the same wave tile
+// the fragment reads and products interleave more finely.
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int BK, int WM, int WN, int NWAVE, int OCC, int STAGES, int GM,
           class Epi>
 __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restrict__ A, long lda,
                                                            const bf16* __restrict__ W, long ldw,
                                                            int M, int N, int K, Epi epi) {
-  typedef Mfma32<bf16> MF;
   constexpr int CH = 8;                       // bf16 per 16-byte chunk
   constexpr int CPR = BK / CH;                // chunks per LDS row
   constexpr int RPI = 64 / CPR;               // rows filled by one wave instruction
@@ -265,15 +329,16 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   constexpr int PER_SLICE = A_INST + B_INST;
   constexpr int STAGE = (BM + BN) * BK;       // elements per stage
   constexpr int WAVES_N = BN / WN;
-  constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int KS = BK / MF::KSTEP;
+  constexpr int TM = WM / 16, TN = WN / 16;  // 16x16 accumulators per wave
+  constexpr int KS = BK / 32;                 // MFMA k-steps per slice
   static_assert(A_INST * RPI * NWAVE == BM && B_INST * RPI * NWAVE == BN, "load split");
   static_assert((BM / WM) * WAVES_N == NWAVE, "wave grid");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
   static_assert(BN * BK * 2 == 32768 && RPI * BK * 2 == 1024, "tiled W block layout");
   __shared__ __attribute__((aligned(1024))) bf16 smem[STAGES * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
   const int tiles_n = (N + BN - 1) / BN;
@@ -329,19 +394,19 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
                         slice * BN * BK * 2);
   };
 
-  f32x16 acc[TM][TN];
-  init_acc_bias(acc, epi.bias, n0 + wn * WN, lane, N);
+  f32x4 acc[TM][TN];
+  init_acc16_bias(acc, epi.bias, n0 + wn * WN, lane, N);
 
   const int nk = K / BK;
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue(s, s);
 
-  // fragment addressing: lane reads row (lane & 31) of each 32-row block at
-  // logical chunk 2*ks + (lane >> 5)
-  const int a_row0 = wm * WM + (lane & 31);
-  const int b_row0 = wn * WN + (lane & 31);
-  const int half = lane >> 5;
+  // fragment addressing (16x16x32 operands): lane reads row (lane & 15) of
+  // each 16-row block at logical chunk 4*ks + (lane >> 4)
+  const int a_row0 = wm * WM + (lane & 15);
+  const int b_row0 = wn * WN + (lane & 15);
+  const int quad = lane >> 4;
 
   for (int kt = 0; kt < nk; ++kt) {
     const int rem = nk - 1 - kt;  // slices requested after slice kt
@@ -352,18 +417,18 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
     const bf16* sa = smem + (kt % STAGES) * STAGE;
     const bf16* sb = sa + BM * BK;
     // fragments of k-step ks+1 are requested before the products of ks
-    typename MF::frag fa[2][TM], fb[2][TN];
+    bf16x8 fa[2][TM], fb[2][TN];
     auto fetch = [&](int ks, int slot) {
-      const int c = 2 * ks + half;
+      const int c = 4 * ks + quad;
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
-        const int r = a_row0 + i * 32;
-        fa[slot][i] = MF::load(sa + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+        const int r = a_row0 + i * 16;
+        fa[slot][i] = *reinterpret_cast<const bf16x8*>(sa + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        const int r = b_row0 + j * 32;
-        fb[slot][j] = MF::load(sb + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+        const int r = b_row0 + j * 16;
+        fb[slot][j] = *reinterpret_cast<const bf16x8*>(sb + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
       }
     };
     fetch(0, 0);
@@ -373,11 +438,12 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = MF::mma(fb[ks & 1][j], fa[ks & 1][i], acc[i][j]);
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[ks & 1][j], fa[ks & 1][i], acc[i][j], 0, 0, 0);
     }
   }
 
-  gemm_epilogue(acc, m0 + wm * WM, n0 + wn * WN, lane, M, N, epi);
+  gemm_epilogue16(acc, m0 + wm * WM, n0 + wn * WN, lane, M, N, epi);
 }
 
 // ------------------------------------------------------------- epilogues

@@ -21,8 +21,8 @@ static hipError_t launch_flash(const AttnArgs<T>& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-// bf16: direct-to-LDS tiles of 64 keys in a 4-deep ring, one 32-query block
-// per wave.
+// bf16, head dim 32: XOR-swizzled direct-to-LDS tiles of 64 keys in a
+// 4-deep ring, one 32-query block per wave.
 template <int DH, int QB, int NW, int OCC>
 static hipError_t launch_flash_dl(const AttnArgs<bf16>& a, hipStream_t st) {
   constexpr int KVT = 64, STAGES = 4;
@@ -40,12 +40,30 @@ static hipError_t launch_flash_dl(const AttnArgs<bf16>& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// bf16, head dims 64 and 128: padded-row tiles of 64 keys in a 4-deep ring
+// (140 KB of LDS at 128), 8 waves of 32 queries.
+template <int DH>
+static hipError_t launch_flash_pad(const AttnArgs<bf16>& a, hipStream_t st) {
+  constexpr int NW = 8, OCC = 2, STAGES = 4;
+  const long nwg = (long)cdiv(a.lq, NW * 32) * a.heads * a.n_streams;
+  if (nwg * 64 * NW > 0xFFFFFFFFL) return hipErrorInvalidConfiguration;
+  if ((long)a.lk * a.k_ld * 2 > 0x7FFFFFFFL || (long)DH * a.vt_ld * 2 > 0x7FFFFFFFL)
+    return hipErrorInvalidValue;
+  if (a.kv_sel)
+    hipLaunchKernelGGL((k_flash_pad<DH, NW, OCC, STAGES, true>), dim3((unsigned)nwg), dim3(64 * NW), 0,
+                       st, a);
+  else
+    hipLaunchKernelGGL((k_flash_pad<DH, NW, OCC, STAGES, false>), dim3((unsigned)nwg), dim3(64 * NW), 0,
+                       st, a);
+  return hipGetLastError();
+}
+
 template <>
 hipError_t flash_attention<bf16>(const AttnArgs<bf16>& a, int head_dim, hipStream_t st) {
   if (a.lq <= 0 || a.n_streams <= 0) return hipSuccess;
   switch (head_dim) {
-    case 128: return launch_flash_dl<128, 1, 8, 2>(a, st);
-    case 64: return launch_flash_dl<64, 1, 8, 2>(a, st);
+    case 128: return launch_flash_pad<128>(a, st);
+    case 64: return launch_flash_pad<64>(a, st);
     case 32: return launch_flash_dl<32, 1, 4, 1>(a, st);
     default: return hipErrorInvalidValue;
   }

@@ -4,8 +4,8 @@
 namespace cs {
 
 // ------------------------------------------------------------- launchers
-// bf16: direct-to-LDS kernel, 256x256 tiles, 8 waves of 128x64 (two per
-//       SIMD), K slices of 64 in two LDS stages (128 KB), tile groups of 4
+// bf16: direct-to-LDS kernel on 16x16x32 MFMAs, 256x256 tiles, 8 waves of
+//       128x64 (two per SIMD), K slices of 64 in two LDS stages (128 KB), tile groups of 4
 //       tile-rows; the fastest shape of those swept at the Wan2.1-1.3B
 //       projection sizes.  K must be a multiple of 64.
 // fp32: register-staged kernel, 128x128 tiles, 4 waves of 64x64, K slices of 16.
