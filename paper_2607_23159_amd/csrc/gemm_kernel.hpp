@@ -16,6 +16,8 @@
 #pragma once
 #include "kernels.hpp"
 
+#include <type_traits>
+
 namespace cs {
 
 template <typename T, int BM, int BN, int BK, int WM, int WN, int NWAVE>
@@ -306,7 +308,8 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
 // stage the tiles and no LDS store instructions are issued.  K slices rotate
 // through a ring of STAGES buffers: slice k+STAGES-1 is requested while slice
 // k is multiplied, and a wave waits (vmcnt) only for slice k before the single
-// barrier of each iteration.  LDS rows are unpadded; the 16-byte chunk c of
+// barrier of each iteration (STAGES = 2: slice k+1 is requested while slice
+// k is multiplied).  LDS rows are unpadded; the 16-byte chunk c of
 // row r is stored at chunk c ^ f(r), f(r) = (r ^ (r >> log2 CPR)) & (CPR-1),
 // which keeps the fragment reads (16 rows x 4 chunks per instruction) free of
 // bank conflicts.
@@ -333,7 +336,8 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   constexpr int KS = BK / 32;                 // MFMA k-steps per slice
   static_assert(A_INST * RPI * NWAVE == BM && B_INST * RPI * NWAVE == BN, "load split");
   static_assert((BM / WM) * WAVES_N == NWAVE, "wave grid");
-  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+  static_assert(STAGES == 2, "two-stage ring");
+  static_assert(KS == 2, "two k-steps per slice");
   static_assert(BN * BK * 2 == 32768 && RPI * BK * 2 == 1024, "tiled W block layout");
   __shared__ __attribute__((aligned(1024))) bf16 smem[STAGES * STAGE];
 
@@ -398,9 +402,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   init_acc16_bias(acc, epi.bias, n0 + wn * WN, lane, N);
 
   const int nk = K / BK;
-#pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(s, s);
+  issue(0, 0);
 
   // fragment addressing (16x16x32 operands): lane reads row (lane & 15) of
   // each 16-row block at logical chunk 4*ks + (lane >> 4)
@@ -408,40 +410,56 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   const int b_row0 = wn * WN + (lane & 15);
   const int quad = lane >> 4;
 
-  for (int kt = 0; kt < nk; ++kt) {
-    const int rem = nk - 1 - kt;  // slices requested after slice kt
-    if (rem >= STAGES - 2) wait_vm_barrier<(STAGES - 2) * PER_SLICE>();
-    else if (STAGES > 3 && rem == 1) wait_vm_barrier<(STAGES > 3 ? 1 : 0) * PER_SLICE>();
-    else wait_vm_barrier<0>();
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-    const bf16* sa = smem + (kt % STAGES) * STAGE;
+  // One slice: wait for it, request the next one into the other stage, then
+  // the products of its two k-steps.  The instruction order inside a slice is
+  // fixed with scheduling groups: the next slice's loads and k-step 0's
+  // fragment reads first, then k-step 0's products with k-step 1's fragment
+  // reads spread among them, then k-step 1's products.  The last slice is
+  // peeled so that each slice is one straight-line block.
+  auto slice = [&](int kt, auto more) {
+    wait_vm_barrier<0>();
+    if constexpr (decltype(more)::value) issue(kt + 1, (kt + 1) & 1);
+    const bf16* sa = smem + (kt & 1) * STAGE;
     const bf16* sb = sa + BM * BK;
-    // fragments of k-step ks+1 are requested before the products of ks
-    bf16x8 fa[2][TM], fb[2][TN];
-    auto fetch = [&](int ks, int slot) {
+    bf16x8 fa[KS][TM], fb[KS][TN];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
       const int c = 4 * ks + quad;
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = a_row0 + i * 16;
-        fa[slot][i] = *reinterpret_cast<const bf16x8*>(sa + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+        fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int r = b_row0 + j * 16;
-        fb[slot][j] = *reinterpret_cast<const bf16x8*>(sb + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+        fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
       }
-    };
-    fetch(0, 0);
+    }
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (ks + 1 < KS) fetch(ks + 1, (ks + 1) & 1);
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[ks & 1][j], fa[ks & 1][i], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
+    // NM / NF products per fragment read (rounded down: with 8 x 4
+    // accumulators, 2 products per read, the rest of k-step 0 and k-step 1
+    // after the reads)
+    constexpr int NF = TM + TN, NM = TM * TN;
+    __builtin_amdgcn_sched_group_barrier(0x020, decltype(more)::value ? PER_SLICE : 0, 0);  // VMEM
+    __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);                                    // DS read
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, NM / NF, 0);                             // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-  }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+  };
+  typedef std::integral_constant<bool, true> More;
+  typedef std::integral_constant<bool, false> Last;
+  for (int kt = 0; kt + 1 < nk; ++kt) slice(kt, More{});
+  slice(nk - 1, Last{});
 
   gemm_epilogue16(acc, m0 + wm * WM, n0 + wn * WN, lane, M, N, epi);
 }

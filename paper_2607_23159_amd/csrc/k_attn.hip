@@ -40,11 +40,11 @@ static hipError_t launch_flash_dl(const AttnArgs<bf16>& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-// bf16, head dims 64 and 128: padded-row tiles of 64 keys in a 4-deep ring
-// (140 KB of LDS at 128), 8 waves of 32 queries.
+// bf16, head dims 64 and 128: padded-row tiles of 64 keys in a 3-deep ring
+// (105 KB of LDS at 128), 12 waves of 32 queries (three per SIMD).
 template <int DH>
 static hipError_t launch_flash_pad(const AttnArgs<bf16>& a, hipStream_t st) {
-  constexpr int NW = 8, OCC = 2, STAGES = 4;
+  constexpr int NW = 12, OCC = 3, STAGES = 3;
   const long nwg = (long)cdiv(a.lq, NW * 32) * a.heads * a.n_streams;
   if (nwg * 64 * NW > 0xFFFFFFFFL) return hipErrorInvalidConfiguration;
   if ((long)a.lk * a.k_ld * 2 > 0x7FFFFFFFL || (long)DH * a.vt_ld * 2 > 0x7FFFFFFFL)
