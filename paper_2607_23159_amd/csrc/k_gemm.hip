@@ -64,7 +64,7 @@ template <typename T, class C, class Epi>
 static hipError_t launch_staged(const T* A, long lda, const T* W, long ldw, int M, int N, int K,
                                 Epi epi, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (K % C::BK != 0 || N % 4 != 0) return hipErrorInvalidValue;
+  if (K <= 0 || K % C::BK != 0 || N % 4 != 0) return hipErrorInvalidValue;
   const long tiles = (long)cdiv(M, C::BM) * cdiv(N, C::BN);
   hipLaunchKernelGGL((k_gemm<T, C::BM, C::BN, C::BK, C::WM, C::WN, C::NW, C::OCC, C::GM, Epi>),
                      dim3((unsigned)tiles), dim3(64 * C::NW), 0, st, A, lda, W, ldw, M, N, K, epi);
@@ -77,7 +77,7 @@ static hipError_t launch(const T* A, long lda, const T* W, long ldw, int M, int 
   if constexpr (sizeof(T) == 2) {
     typedef DlCfg C;
     if (M <= 0 || N <= 0) return hipSuccess;
-    if (K % C::BK != 0 || N % 4 != 0) return hipErrorInvalidValue;
+    if (K <= 0 || K % C::BK != 0 || N % 4 != 0) return hipErrorInvalidValue;
     // W is pre-tiled (row stride K); per-tile buffer ranges are 32-bit byte counts
     if (ldw != K) return hipErrorInvalidValue;
     if ((long)std::max(C::BM, C::BN) * std::max(lda, (long)K) * 2 > 0x7FFFFFFFL) return hipErrorInvalidValue;
