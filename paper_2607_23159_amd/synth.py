@@ -128,6 +128,14 @@ MODELS: Dict[str, ModelCfg] = {
     "wan_mid": ModelCfg(n_blocks=2, hidden=1536, heads=12, head_dim=128,
                         ffn=8960, text_dim=4096, text_len=512, in_ch=16,
                         lat_f=3, lat_h=16, lat_w=32),
+    # Wan2.2-5B and Wan2.1-14B widths, 2 blocks, 384 tokens: the widest
+    # projections (K up to 5120, N up to 15360) and 24 / 40 heads at oracle cost.
+    "wan5b_mid": ModelCfg(n_blocks=2, hidden=3072, heads=24, head_dim=128,
+                          ffn=14336, text_dim=4096, text_len=512, in_ch=48,
+                          lat_f=3, lat_h=16, lat_w=32),
+    "wan14b_mid": ModelCfg(n_blocks=2, hidden=5120, heads=40, head_dim=128,
+                           ffn=13824, text_dim=4096, text_len=512, in_ch=16,
+                           lat_f=3, lat_h=16, lat_w=32),
     # One Wan2.1-1.3B block at the full 32,760-token latent.
     "wan13b_block1": ModelCfg(**dict(_WAN13B, n_blocks=1)),
     "wan13b": ModelCfg(**_WAN13B),

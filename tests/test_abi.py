@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     B.lib()  # loads and binds every signature
 
 
-@pytest.mark.parametrize("name", ["tiny", "wan_mid", "wan13b", "wan5b", "wan14b"])
+@pytest.mark.parametrize("name", ["tiny", "wan_mid", "wan5b_mid", "wan14b_mid", "wan13b", "wan5b", "wan14b"])
 def test_weight_count_matches_generator_layout(name):
     m = synth.MODELS[name]
     assert B.cs_model_weight_count(B.model_desc(m)) == synth.weight_count(m)

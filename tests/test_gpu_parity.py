@@ -1,7 +1,8 @@
 """GPU parity: the HIP path (through the C ABI) against the float64 oracle.
 
-Velocity parity per model shape (tiny, Wan widths at 384 tokens, one
-Wan2.1-1.3B block at the full 32,760 tokens on sampled tokens), rollout
+Velocity parity per model shape (tiny, Wan2.1-1.3B, Wan2.2-5B and
+Wan2.1-14B widths at 384 tokens, one Wan2.1-1.3B block at the full 32,760
+tokens on sampled tokens), rollout
 parity (schedules, latents, scores, rankings) on the tiny workload for
 fp32 and bf16, one and two guidance branches and tau in
 {0, 0.05, 0.1, 0.2, inf}, and a Wan-width rollout."""
@@ -84,6 +85,28 @@ def test_velocity_wan_mid_bf16(init):
         err = rel_l2(v[i], odit.velocity(x[i], 0.7, emb, W, m))
         say(f"  i={i} rel_l2={err:.3e}")
         assert err < TOL[0] / 2
+
+
+@pytest.mark.parametrize("name", ["wan5b_mid", "wan14b_mid"])
+def test_velocity_wide_models_bf16(name):
+    """Wan2.2-5B and Wan2.1-14B widths (d = 3072 / 5120, 24 / 40 heads, FFN
+    14336 / 13824, 2 blocks, 384 tokens): the widest projections and head
+    counts the workloads use, against the oracle."""
+    say(f"velocity {name} bf16 stress init")
+    m = synth.MODELS[name].with_dtype(synth.DTYPE_BF16)
+    flat = synth.make_weights(m, init="stress")
+    W = {k: v.astype(np.float64) for k, v in synth.unflatten(m, flat).items()}
+    gm = GpuModel(m, flat)
+    try:
+        x = synth.make_noise(m, 1, seed0=650)
+        ctx = synth.make_context(m, 1)
+        v = gm.velocity(torch.from_numpy(x.reshape(1, -1)).cuda(), 0.6, torch.from_numpy(ctx).cuda())
+        v = v.cpu().numpy().reshape(x.shape)
+        err = rel_l2(v[0], odit.velocity(x[0], 0.6, odit.text_embedding(ctx, W), W, m))
+        say(f"  rel_l2={err:.3e}")
+        assert err < TOL[0] / 2
+    finally:
+        gm.close()
 
 
 def test_velocity_full_length_block_sampled():
