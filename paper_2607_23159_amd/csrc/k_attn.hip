@@ -31,6 +31,7 @@ static hipError_t launch_flash_dl(const AttnArgs<bf16>& a, hipStream_t st) {
   // buffer ranges and offsets are 32-bit byte counts
   if ((long)a.lk * a.k_ld * 2 > 0x7FFFFFFFL || (long)DH * a.vt_ld * 2 > 0x7FFFFFFFL)
     return hipErrorInvalidValue;
+  if (a.vt_ld < round_up(a.lk, KVT)) return hipErrorInvalidValue;
   if (a.kv_sel)
     hipLaunchKernelGGL((k_flash_dl<DH, QB, KVT, NW, OCC, STAGES, true>), dim3((unsigned)nwg),
                        dim3(64 * NW), 0, st, a);
@@ -49,6 +50,8 @@ static hipError_t launch_flash_pad(const AttnArgs<bf16>& a, hipStream_t st) {
   if (nwg * 64 * NW > 0xFFFFFFFFL) return hipErrorInvalidConfiguration;
   if ((long)a.lk * a.k_ld * 2 > 0x7FFFFFFFL || (long)DH * a.vt_ld * 2 > 0x7FFFFFFFL)
     return hipErrorInvalidValue;
+  // every 64-key tile of V^T must lie inside its padded row
+  if (a.vt_ld < round_up(a.lk, 64)) return hipErrorInvalidValue;
   if (a.kv_sel)
     hipLaunchKernelGGL((k_flash_pad<DH, NW, OCC, STAGES, true>), dim3((unsigned)nwg), dim3(64 * NW), 0,
                        st, a);
