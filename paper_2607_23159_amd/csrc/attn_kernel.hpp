@@ -196,7 +196,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash(AttnArgs<T> a) {
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][qb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * a.scale_log2;
+      mx = max_lane_pair32(mx) * a.scale_log2;
       if (__any(mx > m_run[qb] + RESCALE_LOG2)) {
         const float m_new = fmaxf(m_run[qb], mx);
         const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
@@ -453,7 +453,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash_dl(AttnArgs<bf16> a) {
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][qb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * a.scale_log2;
+      mx = max_lane_pair32(mx) * a.scale_log2;
       if (__any(mx > m_run[qb] + RESCALE_LOG2)) {
         const float m_new = fmaxf(m_run[qb], mx);
         const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
@@ -687,7 +687,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_flash_pad(AttnArgs<bf16> a) {
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * a.scale_log2;
+    mx = max_lane_pair32(mx) * a.scale_log2;
     if (__any(mx > m_run + RESCALE_LOG2)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);

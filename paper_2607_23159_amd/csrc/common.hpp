@@ -82,6 +82,13 @@ CS_DEV double wave_sum(double v) {
   return v;
 }
 
+// Maximum of x over lanes l and l ^ 32.  v_permlane32_swap exchanges the two
+// 32-lane halves inside the VALU (no LDS round trip, unlike a shuffle).
+CS_DEV float max_lane_pair32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // The dispatcher deals workgroups round-robin to the 8 XCDs, each with its
 // own L2.  This maps a hardware workgroup id to a virtual id so that every
 // XCD runs one contiguous range of virtual ids (a bijection on [0, nwg) for
