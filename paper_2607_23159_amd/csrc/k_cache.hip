@@ -5,9 +5,9 @@
 // skipped iff a_s <= tau, else it computes and a_s resets to 0.  The two
 // sums are reduced in fp64, first per (candidate, 8192-element chunk) by a
 // coalesced streaming kernel that reads x once for all branches, then per
-// stream in chunk order by a one-wave kernel that also compacts the list of
-// computing streams with a ballot (no atomics: results do not depend on
-// timing).
+// stream by one wave each (strided over the chunks, then a fixed butterfly),
+// and a single wave takes the decisions and compacts the list of computing
+// streams with a ballot (no atomics: results do not depend on timing).
 //
 // Update: skipped streams use x + Delta (Eq. skip); computed streams take
 // the transformer output v and, when the cache is on, refresh Delta = v - x
@@ -74,7 +74,24 @@ hipError_t decide_partials(const float* x, const float* xref, int n_cand, int n_
   return hipGetLastError();
 }
 
-__global__ __launch_bounds__(64) void k_decide_finalize(DecideParams p,
+// Per-stream totals of the chunk partials, one wave per stream: lane l sums
+// chunks l, l + 64, ... in order, then the lanes combine in a fixed butterfly
+// (the order depends only on the chunk count, never on timing).
+CS_DEV void wave_stream_sums(const double* __restrict__ ps, int nchunk, double& num, double& den) {
+  const int lane = threadIdx.x & 63;
+  double n = 0.0, d = 0.0;
+  for (int c = lane; c < nchunk; c += 64) {
+    const double2 v = reinterpret_cast<const double2*>(ps)[c];
+    n += v.x;
+    d += v.y;
+  }
+  num = wave_sum(n);
+  den = wave_sum(d);
+}
+
+constexpr int FIN_WAVES = 16;
+
+__global__ __launch_bounds__(64 * FIN_WAVES) void k_decide_finalize(DecideParams p,
                                                          const double* __restrict__ partials,
                                                          const uint8_t* __restrict__ ovr,
                                                          double* __restrict__ a,
@@ -84,7 +101,20 @@ __global__ __launch_bounds__(64) void k_decide_finalize(DecideParams p,
                                                          int32_t* __restrict__ slots,
                                                          int32_t* __restrict__ branch,
                                                          DecideOut* __restrict__ out) {
-  const int lane = threadIdx.x;
+  __shared__ double sums[2 * MAX_DECIDE_STREAMS];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (p.use_partials) {
+    for (int s = wave; s < p.n_streams; s += FIN_WAVES) {
+      double num, den;
+      wave_stream_sums(partials + (long)s * p.nchunk * 2, p.nchunk, num, den);
+      if (lane == 0) {
+        sums[2 * s] = num;
+        sums[2 * s + 1] = den;
+      }
+    }
+  }
+  __syncthreads();
+  if (wave != 0) return;
   int count = 0;
   for (int base = 0; base < p.n_streams; base += 64) {
     const int s = base + lane;
@@ -98,12 +128,7 @@ __global__ __launch_bounds__(64) void k_decide_finalize(DecideParams p,
         if (p.mode == 2) {
           compute = ((p.step - p.k_warm) % p.static_k) == 0;
         } else if (p.use_partials) {
-          double num = 0.0, den = 0.0;
-          const double* ps = partials + (long)s * p.nchunk * 2;
-          for (int c = 0; c < p.nchunk; ++c) {
-            num += ps[2 * c];
-            den += ps[2 * c + 1];
-          }
+          const double num = sums[2 * s], den = sums[2 * s + 1];
           if (den > 0.0) {
             a[s] += sqrt(num) / sqrt(den);
             seen = a[s];
@@ -133,7 +158,8 @@ __global__ __launch_bounds__(64) void k_decide_finalize(DecideParams p,
 hipError_t decide_finalize(const DecideParams& p, const double* partials, const uint8_t* ovr,
                            double* a, uint8_t* has_ref, uint8_t* mask, double* a_seen,
                            int32_t* slots, int32_t* branch, DecideOut* out, hipStream_t st) {
-  hipLaunchKernelGGL(k_decide_finalize, dim3(1), dim3(64), 0, st, p, partials, ovr, a, has_ref,
+  if (p.n_streams > MAX_DECIDE_STREAMS) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_decide_finalize, dim3(1), dim3(64 * FIN_WAVES), 0, st, p, partials, ovr, a, has_ref,
                      mask, a_seen, slots, branch, out);
   return hipGetLastError();
 }
@@ -225,19 +251,23 @@ hipError_t score_partials(const float* x, const float* vt, float c, const float*
   return hipGetLastError();
 }
 
-__global__ void k_score_finalize(const double* __restrict__ partials, int n_cand, int nchunk,
-                                 double inv_sqrt_d, double* __restrict__ scores) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n_cand) return;
+// One wave per candidate, the same fixed order as the decision totals.
+__global__ __launch_bounds__(64) void k_score_finalize(const double* __restrict__ partials,
+                                                       int nchunk, double inv_sqrt_d,
+                                                       double* __restrict__ scores) {
+  const int i = blockIdx.x, lane = threadIdx.x;
+  const double* ps = partials + (long)i * nchunk;
   double s = 0.0;
-  for (int c = 0; c < nchunk; ++c) s += partials[(long)i * nchunk + c];
-  scores[i] = s * inv_sqrt_d;
+  for (int c = lane; c < nchunk; c += 64) s += ps[c];
+  s = wave_sum(s);
+  if (lane == 0) scores[i] = s * inv_sqrt_d;
 }
 
 hipError_t score_finalize(const double* partials, int n_cand, int nchunk, long D, double* scores,
                           hipStream_t st) {
-  hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)cdiv(n_cand, 64)), dim3(64), 0, st, partials,
-                     n_cand, nchunk, 1.0 / sqrt((double)D), scores);
+  if (n_cand <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)n_cand), dim3(64), 0, st, partials, nchunk,
+                     1.0 / sqrt((double)D), scores);
   return hipGetLastError();
 }
 

@@ -92,6 +92,9 @@ hipError_t decide_partials(const float* x, const float* xref, int n_cand, int n_
                            double* partials, hipStream_t st);
 // Finalize: per stream s = i*B + b, forced / rule / override -> mask, a_seen,
 // compact list of computed streams and their branches, count.
+// Streams (candidates x branches) one decision launch handles: 1024
+// candidates with two branches each.
+constexpr int MAX_DECIDE_STREAMS = 2048;
 struct DecideParams {
   int n_streams, n_branch, step, n_steps, k_warm, k_cool, mode, static_k, nchunk;
   int use_partials, use_override;
