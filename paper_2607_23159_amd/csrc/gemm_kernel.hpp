@@ -119,6 +119,14 @@ CS_DEV void gemm_epilogue(const f32x16 (&acc)[TM][TN], int row_base, int col_bas
 // formed as C^T tiles: accumulator (i, j) of a lane holds row i*16 + lane%16
 // of the wave's sub-tile and, in registers 0..3, columns j*16 + 4(lane/16) ..
 // +3, one vector access in the epilogue.
+// LDS layout of the direct-load bf16 kernels: a tile row holds 64 bf16 (8
+// chunks of 16 bytes); logical chunk c of row r is stored at c ^ gemm_swz(r).
+// The swizzle has a period of 16 rows: the 16 rows one fragment read covers
+// (each reading one logical chunk) land in 16 distinct 16-byte bank groups,
+// and rows r and r + 16 share the swizzle, so the fragment reads of the
+// 16-row blocks of a wave tile differ by an immediate offset.
+CS_DEV int gemm_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
 template <int TM, int TN>
 CS_DEV void init_acc16_bias(f32x4 (&acc)[TM][TN], const float* __restrict__ bias, int col_base,
                             int lane, int N) {
@@ -309,10 +317,9 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm(const T* __restrict__ 
 // through a ring of STAGES buffers: slice k+STAGES-1 is requested while slice
 // k is multiplied, and a wave waits (vmcnt) only for slice k before the single
 // barrier of each iteration (STAGES = 2: slice k+1 is requested while slice
-// k is multiplied).  LDS rows are unpadded; the 16-byte chunk c of
-// row r is stored at chunk c ^ f(r), f(r) = (r ^ (r >> log2 CPR)) & (CPR-1),
-// which keeps the fragment reads (16 rows x 4 chunks per instruction) free of
-// bank conflicts.
+// k is multiplied).  LDS rows are unpadded and swizzled (gemm_swz), which
+// keeps the fragment reads (16 rows x 4 chunks per instruction) free of bank
+// conflicts.
 //
 // The 16x16x32 product gives bitwise the same sums as two chained 32x32x16
 // steps over the same K order (checked at all projection shapes), and measured
@@ -381,7 +388,7 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
 #pragma unroll
     for (int i = 0; i < A_INST; ++i) {
       const int row = (wave * A_INST + i) * RPI + rin;
-      a_off[i] = (row * (int)lda + (phys ^ chunk_swz<CPR>(row)) * CH) * 2;
+      a_off[i] = (row * (int)lda + (phys ^ gemm_swz(row)) * CH) * 2;
     }
 #pragma unroll
     for (int i = 0; i < B_INST; ++i) b_off[i] = (wave * B_INST + i) * 1024 + lane * 16;
@@ -428,12 +435,12 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = a_row0 + i * 16;
-        fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+        fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + r * BK + (c ^ gemm_swz(r)) * CH);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int r = b_row0 + j * 16;
-        fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + r * BK + (c ^ chunk_swz<CPR>(r)) * CH);
+        fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + r * BK + (c ^ gemm_swz(r)) * CH);
       }
     }
 #pragma unroll
@@ -462,6 +469,252 @@ __global__ __launch_bounds__(64 * NWAVE, OCC) void k_gemm_dl(const bf16* __restr
   slice(nk - 1, Last{});
 
   gemm_epilogue16(acc, m0 + wm * WM, n0 + wn * WN, lane, M, N, epi);
+}
+
+// Epilogue over 16x16 accumulators with the epilogue operands of PD - 1
+// chunks in flight (a ring of PD slots): with one wave per SIMD nothing else
+// hides the latency of the residual reads, so they are requested well ahead.
+template <bool CHECK, int PD, int TM, int TN, class Epi>
+CS_DEV void gemm_epilogue16_deep_impl(const f32x4 (&acc)[TM][TN], int row_base, int col_base,
+                                      int lane, int M, int N, const Epi& epi) {
+  constexpr int NQ = TM * TN;
+  typename Epi::Pre pre[PD];
+  auto fetch = [&](int q) {
+    const int i = q / TN, j = q % TN;
+    const int row = row_base + i * 16 + (lane & 15);
+    const int col0 = col_base + j * 16 + 4 * (lane >> 4);
+    if (!CHECK || (row < M && col0 < N)) pre[q % PD] = epi.pre(row, col0);
+  };
+#pragma unroll
+  for (int q = 0; q < PD - 1 && q < NQ; ++q) fetch(q);
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    if (q + PD - 1 < NQ) fetch(q + PD - 1);
+    const int i = q / TN, j = q % TN;
+    const int row = row_base + i * 16 + (lane & 15);
+    const int col0 = col_base + j * 16 + 4 * (lane >> 4);
+    if (!CHECK || (row < M && col0 < N)) {
+      const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      epi(row, col0, v, pre[q % PD]);
+    }
+  }
+}
+
+template <int PD, int TM, int TN, class Epi>
+CS_DEV void gemm_epilogue16_deep(const f32x4 (&acc)[TM][TN], int row_base, int col_base, int lane,
+                                 int M, int N, const Epi& epi) {
+  if (row_base + TM * 16 <= M && col_base + TN * 16 <= N)
+    gemm_epilogue16_deep_impl<false, PD>(acc, row_base, col_base, lane, M, N, epi);
+  else
+    gemm_epilogue16_deep_impl<true, PD>(acc, row_base, col_base, lane, M, N, epi);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 GEMM, one wave per SIMD: BM x 256 tiles (BM = 256 or 192), 4 waves of
+// (BM/2) x 128 (16x16x32 MFMAs; BM/2 x 128 / 64 accumulator registers per
+// lane, held in AGPRs).
+//
+// Fragment reads from LDS per product: (BM/32 + 8) reads per BM/4 products,
+// against 12 per 32 with 8 waves of 128x64, so the LDS, which also absorbs
+// the direct loads, is less of a co-limit.  With a single wave per SIMD no
+// other wave hides a stall, so every LDS read is issued half a K slice (one
+// k-step of products) ahead of its use, and the direct loads are spread
+// evenly over the slice (clumped, they back up the address unit and stall
+// the issuing wave):
+//
+//   slice k, half 1: products of k-step 0 | reads of k-step 1 of slice k |
+//                    loads of the A rows of slice k+2
+//   wait: own loads of slice k+1 landed, own reads done; barrier
+//   slice k, half 2: products of k-step 1 | reads of k-step 0 of slice k+1 |
+//                    loads of the W rows of slice k+2
+//
+// A tiles rotate through three LDS buffers and W tiles through two (160 KB
+// at BM = 256): the A buffer of slice k+2 held slice k-1, which every wave
+// finished reading before the previous barrier, and the W buffer of slice
+// k+2 held slice k, whose last reads precede this slice's barrier.
+//
+// The products are issued as volatile inline assembly with the accumulators
+// bound to AGPRs: that fixes the issue order exactly (LDS reads and loads
+// are ordered against them) and keeps the register allocator from moving
+// accumulators between the register files.  The compiler does not see them
+// as matrix instructions, so the hazards it would otherwise cover are
+// covered here: the accumulators are written (bias) long before the first
+// product, and none is read until 24 wait states after the last product.
+//
+// Same LDS row layout, tiled weights, tile order and accumulation order over
+// K as k_gemm_dl: results are bitwise equal to it.
+// ---------------------------------------------------------------------------
+CS_DEV void mfma_16x16x32_agpr(f32x4& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+template <int BM, int GM, int PD, class Epi>
+__global__ __launch_bounds__(256, 1) void k_gemm_w4(const bf16* __restrict__ A, long lda,
+                                                  const bf16* __restrict__ W, long ldw, int M,
+                                                  int N, int K, Epi epi) {
+  constexpr int BN = 256, BK = 64, NWAVE = 4, WM = BM / 2, WN = 128;
+  constexpr int CH = 8;                       // bf16 per 16-byte chunk
+  constexpr int CPR = BK / CH;                // chunks per LDS row
+  constexpr int RPI = 64 / CPR;               // rows filled by one wave instruction
+  constexpr int A_INST = BM / RPI / NWAVE;    // load instructions per wave per slice
+  constexpr int B_INST = BN / RPI / NWAVE;
+  constexpr int A_BUF = BM * BK, B_BUF = BN * BK;  // elements per buffer
+  constexpr int WAVES_N = BN / WN;
+  constexpr int TM = WM / 16, TN = WN / 16;
+  constexpr int NF = TM + TN, NM = TM * TN;   // reads and products per k-step
+  constexpr int RPM = 3;                      // products per read
+  static_assert(BM == 256 || BM == 192, "tile rows");
+  static_assert(A_INST * RPI * NWAVE == BM && B_INST * RPI * NWAVE == BN, "load split");
+  static_assert(BN * BK * 2 == 32768 && RPI * BK * 2 == 1024, "tiled W block layout");
+  static_assert(RPM * (NF - 1) < NM && NM % A_INST == 0 && NM % B_INST == 0, "interleave");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[3 * A_BUF + 2 * B_BUF];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+  const int tiles_n = (N + BN - 1) / BN;
+  const int tiles_m = (M + BM - 1) / BM;
+  const int bid = xcd_contiguous(blockIdx.x, gridDim.x);
+  int tm_i, tn_i;
+  if (GM > 1) {
+    const int group = bid / (GM * tiles_n);
+    const int first_m = group * GM;
+    const int gm = min(tiles_m - first_m, GM);
+    const int in = bid - group * GM * tiles_n;
+    tm_i = first_m + in % gm;
+    tn_i = in / gm;
+  } else {
+    tm_i = bid / tiles_n;
+    tn_i = bid % tiles_n;
+  }
+  const int m0 = tm_i * BM, n0 = tn_i * BN;
+
+  const bf16* a_base = A + (long)m0 * lda;
+  const bf16* b_base = W + (long)tn_i * BN * K;
+  const int a_bytes = min(BM, M - m0) * (int)lda * 2, b_bytes = BN * K * 2;
+  int a_off[A_INST], b_off[B_INST];
+  {
+    const int rin = lane / CPR, phys = lane % CPR;
+#pragma unroll
+    for (int i = 0; i < A_INST; ++i) {
+      const int row = (wave * A_INST + i) * RPI + rin;
+      a_off[i] = (row * (int)lda + (phys ^ gemm_swz(row)) * CH) * 2;
+    }
+#pragma unroll
+    for (int i = 0; i < B_INST; ++i) b_off[i] = (wave * B_INST + i) * 1024 + lane * 16;
+  }
+  bf16* const sb0 = smem + 3 * A_BUF;
+  // load instruction r of the A (W) rows of slice `slice` into A buffer ab (W buffer bb)
+  auto load_a = [&](int r, int slice, int ab) {
+    buffer_load_lds16(a_base, a_bytes, smem + ab * A_BUF + (wave * A_INST + r) * RPI * BK, a_off[r],
+                      slice * BK * 2);
+  };
+  auto load_b = [&](int r, int slice, int bb) {
+    buffer_load_lds16(b_base, b_bytes, sb0 + bb * B_BUF + (wave * B_INST + r) * RPI * BK, b_off[r],
+                      slice * BN * BK * 2);
+  };
+
+  f32x4 acc[TM][TN];
+  init_acc16_bias(acc, epi.bias, n0 + wn * WN, lane, N);
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) asm volatile("" : "+a"(acc[i][j]));  // in AGPRs from here on
+
+  // fragment addressing (16x16x32 operands): lane reads row (lane & 15) of
+  // each 16-row block at logical chunk 4*ks + (lane >> 4); the swizzle of
+  // row r + 16i equals that of row r, so block i is at an immediate offset
+  const int a_row0 = wm * WM + (lane & 15);
+  const int b_row0 = wn * WN + (lane & 15);
+  const int quad = lane >> 4;
+  const int a_lds[2] = {a_row0 * BK + (quad ^ gemm_swz(a_row0)) * CH,
+                        a_row0 * BK + ((4 + quad) ^ gemm_swz(a_row0)) * CH};
+  const int b_lds[2] = {b_row0 * BK + (quad ^ gemm_swz(b_row0)) * CH,
+                        b_row0 * BK + ((4 + quad) ^ gemm_swz(b_row0)) * CH};
+  // read r (< NF) of k-step ks from A buffer ab / W buffer bb: W fragments
+  // first (the first products of the next half use all of them)
+  auto read = [&](int r, int ab, int bb, int ks, bf16x8(&fa)[TM], bf16x8(&fb)[TN]) {
+    if (r < TN)
+      fb[r] = *reinterpret_cast<const bf16x8*>(sb0 + bb * B_BUF + b_lds[ks] + r * 16 * BK);
+    else
+      fa[r - TN] = *reinterpret_cast<const bf16x8*>(smem + ab * A_BUF + a_lds[ks] + (r - TN) * 16 * BK);
+  };
+
+  bf16x8 f0a[TM], f0b[TN], f1a[TM], f1b[TN];
+  // One half: the NM products of (pa, pb); after product RPM*r, read r into
+  // (na, nb) (RD); NL loads spread evenly, through `ld` (LD).
+  auto half = [&](auto rd, auto ldf, auto nl, const bf16x8(&pa)[TM], const bf16x8(&pb)[TN],
+                  bf16x8(&na)[TM], bf16x8(&nb)[TN], int ab, int bb, int ks) {
+    constexpr int NL = decltype(nl)::value;
+#pragma unroll
+    for (int q = 0; q < NM; ++q) {
+      mfma_16x16x32_agpr(acc[q / TN][q % TN], pb[q % TN], pa[q / TN]);
+      if constexpr (NL > 0) {
+        if (q % (NM / NL) == NM / NL / 2) ldf(q / (NM / NL));
+      }
+      if constexpr (decltype(rd)::value) {
+        if (q % RPM == 0 && q / RPM < NF) read(q / RPM, ab, bb, ks, na, nb);
+      }
+    }
+  };
+  typedef std::integral_constant<bool, true> Y;
+  typedef std::integral_constant<bool, false> F;
+  typedef std::integral_constant<int, 0> L0;
+  typedef std::integral_constant<int, A_INST> LA;
+  typedef std::integral_constant<int, B_INST> LB;
+  auto no_load = [](int) {};
+
+  const int nk = K / BK;
+#pragma unroll
+  for (int r = 0; r < A_INST; ++r) load_a(r, 0, 0);
+#pragma unroll
+  for (int r = 0; r < B_INST; ++r) load_b(r, 0, 0);
+  if (nk > 1) {
+#pragma unroll
+    for (int r = 0; r < A_INST; ++r) load_a(r, 1, 1);
+#pragma unroll
+    for (int r = 0; r < B_INST; ++r) load_b(r, 1, 1);
+    wait_vm_barrier<A_INST + B_INST>();   // slice 0 landed (slice 1 may be in flight)
+  } else {
+    wait_vm_barrier<0>();
+  }
+#pragma unroll
+  for (int r = 0; r < NF; ++r) read(r, 0, 0, 0, f0a, f0b);
+
+  // HN: slice k+1 exists (barrier, its k-step 0 reads); IS: slice k+2
+  // exists (its loads).  Slice k uses A buffer k % 3 and W buffer k % 2.
+  auto slice = [&](int kt, int a3, auto hn, auto is) {
+    const int b2 = kt & 1;
+    const int a_next = a3 == 2 ? 0 : a3 + 1, a_far = a3 == 0 ? 2 : a3 - 1;
+    if constexpr (decltype(is)::value) {
+      half(Y{}, [&](int r) { load_a(r, kt + 2, a_far); }, LA{}, f0a, f0b, f1a, f1b, a3, b2, 1);
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(A_INST) : "memory");
+      half(Y{}, [&](int r) { load_b(r, kt + 2, b2); }, LB{}, f1a, f1b, f0a, f0b, a_next, b2 ^ 1, 0);
+    } else if constexpr (decltype(hn)::value) {
+      half(Y{}, no_load, L0{}, f0a, f0b, f1a, f1b, a3, b2, 1);
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      half(Y{}, no_load, L0{}, f1a, f1b, f0a, f0b, a_next, b2 ^ 1, 0);
+    } else {
+      half(Y{}, no_load, L0{}, f0a, f0b, f1a, f1b, a3, b2, 1);
+      half(F{}, no_load, L0{}, f1a, f1b, f0a, f0b, 0, 0, 0);
+    }
+  };
+  int kt = 0, a3 = 0;
+  for (; kt + 2 < nk; ++kt, a3 = a3 == 2 ? 0 : a3 + 1) slice(kt, a3, Y{}, Y{});
+  if (kt + 1 < nk) {
+    slice(kt, a3, Y{}, F{});
+    ++kt;
+    a3 = a3 == 2 ? 0 : a3 + 1;
+  }
+  slice(kt, a3, F{}, F{});
+
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) asm volatile("" : "+a"(acc[i][j]));  // read only after the nops
+  gemm_epilogue16_deep<PD>(acc, m0 + wm * WM, n0 + wn * WN, lane, M, N, epi);
 }
 
 // ------------------------------------------------------------- epilogues

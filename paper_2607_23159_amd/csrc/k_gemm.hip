@@ -4,10 +4,11 @@
 namespace cs {
 
 // ------------------------------------------------------------- launchers
-// bf16: direct-to-LDS kernel on 16x16x32 MFMAs, 256x256 tiles, 8 waves of
-//       128x64 (two per SIMD), K slices of 64 in two LDS stages (128 KB), tile groups of 4
-//       tile-rows; the fastest shape of those swept at the Wan2.1-1.3B
-//       projection sizes.  K must be a multiple of 64.
+// bf16: direct-to-LDS kernels on 16x16x32 MFMAs, 256x256 tiles, K slices of
+//       64, tile groups of 4 tile-rows: k_gemm_w4 (4 waves of 128x128, one
+//       per SIMD) and, for residual updates at short K, k_gemm_dl (8 waves
+//       of 128x64, two per SIMD).  Both sum in the same order (bitwise
+//       equal results).  K must be a multiple of 64.
 // fp32: register-staged kernel, 128x128 tiles, 4 waves of 64x64, K slices of 16.
 // Narrow N (head GEMM, N = patch_dim): register-staged 128x64 tiles.
 template <typename T> struct GemmCfg;
@@ -31,7 +32,7 @@ struct DlCfg {
 // blocks of DlCfg::BN rows x DlCfg::BK columns, block (tn, kt) at
 // ((tn * K/BK + kt) * BN * BK) elements; inside a block row r holds its 8
 // chunks of 8 columns with logical chunk c at physical position
-// c ^ chunk_swz(r), the LDS layout of the kernel.  Rows past N are zero.
+// c ^ gemm_swz(r), the LDS layout of the kernel.  Rows past N are zero.
 __global__ __launch_bounds__(256) void k_tile_weight(const float* __restrict__ src, int N, int K,
                                                      bf16* __restrict__ dst, long n_chunks) {
   constexpr int BN = DlCfg::BN, BK = DlCfg::BK, CPR = BK / 8;
@@ -43,7 +44,7 @@ __global__ __launch_bounds__(256) void k_tile_weight(const float* __restrict__ s
   const int nk = K / BK;
   const int tn = (int)(blk / nk), kt = (int)(blk % nk);
   const int n = tn * BN + r;
-  const int k0 = kt * BK + (p ^ chunk_swz<CPR>(r)) * 8;
+  const int k0 = kt * BK + (p ^ gemm_swz(r)) * 8;
   bf16x8 v;
 #pragma unroll
   for (int e = 0; e < 8; ++e) v[e] = n < N ? (bf16)src[(long)n * K + k0 + e] : (bf16)0.0f;
@@ -71,6 +72,14 @@ static hipError_t launch_staged(const T* A, long lda, const T* W, long ldw, int 
   return hipGetLastError();
 }
 
+// Residual-update epilogues read and write the fp32 residual stream: at
+// short K their epilogue, not the products, sets the pace, and eight waves
+// per CU (k_gemm_dl) keep more of those reads in flight than four.
+template <class Epi> struct EpiIsResidual : std::false_type {};
+template <int G> struct EpiIsResidual<EpiResidual<G>> : std::true_type {};
+template <int G, typename T> struct EpiIsResidual<EpiResidualStore<G, T>> : std::true_type {};
+constexpr int W4_MIN_RESIDUAL_K = 2048;
+
 template <typename T, class Epi>
 static hipError_t launch(const T* A, long lda, const T* W, long ldw, int M, int N, int K, Epi epi,
                          hipStream_t st) {
@@ -82,8 +91,14 @@ static hipError_t launch(const T* A, long lda, const T* W, long ldw, int M, int 
     if (ldw != K) return hipErrorInvalidValue;
     if ((long)std::max(C::BM, C::BN) * std::max(lda, (long)K) * 2 > 0x7FFFFFFFL) return hipErrorInvalidValue;
     const long tiles = (long)cdiv(M, C::BM) * cdiv(N, C::BN);
-    hipLaunchKernelGGL((k_gemm_dl<C::BM, C::BN, C::BK, C::WM, C::WN, C::NW, C::OCC, C::ST, C::GM, Epi>),
-                       dim3((unsigned)tiles), dim3(64 * C::NW), 0, st, A, lda, W, ldw, M, N, K, epi);
+    if (EpiIsResidual<Epi>::value && K <= W4_MIN_RESIDUAL_K) {
+      hipLaunchKernelGGL((k_gemm_dl<C::BM, C::BN, C::BK, C::WM, C::WN, C::NW, C::OCC, C::ST, C::GM, Epi>),
+                         dim3((unsigned)tiles), dim3(64 * C::NW), 0, st, A, lda, W, ldw, M, N, K, epi);
+    } else {
+      constexpr int PD = EpiIsResidual<Epi>::value ? 8 : 2;
+      hipLaunchKernelGGL((k_gemm_w4<C::BM, C::GM, PD, Epi>), dim3((unsigned)tiles), dim3(256), 0, st, A,
+                         lda, W, ldw, M, N, K, epi);
+    }
     return hipGetLastError();
   } else {
     return launch_staged<T, GemmCfg<T>>(A, lda, W, ldw, M, N, K, epi, st);
