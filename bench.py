@@ -224,7 +224,9 @@ def main():
         scores, c, n = rollout(label="timed")
         computed += c
         calls += n
-        if ref_scores is not None:
+        if N < 2:
+            pass                     # one candidate: nothing to rank (cs_rank needs n >= 2)
+        elif ref_scores is not None:
             _, _, rho, top1 = B.cs_rank(scores, ref_scores)
         else:
             B.cs_rank(scores, scores)
@@ -308,7 +310,7 @@ def main():
         dt_s = time.perf_counter() - t1
         rec = {"tau": tv, "candidate_steps_per_s": round(N * T / dt_s, 4),
                "skip_fraction": round(1 - st.computed / st.calls, 4), "ms_per_rollout": round(dt_s * 1e3, 1)}
-        if ref_scores is not None:
+        if ref_scores is not None and N >= 2:
             _, _, rho_t, top1_t = B.cs_rank(sc, ref_scores)
             rec.update({"rho_vs_full": rho_t, "top1_vs_full": top1_t,
                         "regret": float(max(ref_scores) - ref_scores[int(np.argmax(sc))])})

@@ -42,16 +42,31 @@ static hipError_t launch_flash_dl(const AttnArgs<bf16>& a, hipStream_t st) {
 }
 
 // bf16, head dims 64 and 128: padded-row tiles of 64 keys in a 3-deep ring
-// (105 KB of LDS at 128), 12 waves of 32 queries (three per SIMD).
-template <int DH>
-static hipError_t launch_flash_pad(const AttnArgs<bf16>& a, hipStream_t st) {
-  constexpr int NW = 12, OCC = 3, STAGES = 3;
+// (105 KB of LDS at 128: one workgroup per CU), 32 queries per wave.  Twelve
+// waves (three per SIMD) are the faster shape per query; eight waves (two per
+// SIMD) take 256 instead of 384 queries per workgroup, which matters when the
+// grid is a few rounds of the CUs long: at one 32,760-token stream of 12 heads,
+// 1032 twelve-wave workgroups fill 256 CUs 4.03 times (five rounds) while 1536
+// eight-wave ones fill them exactly six times.  Each wave's arithmetic is the
+// same in both shapes (same key order, same per-wave rescale decisions), so
+// the outputs are bitwise equal and the choice never changes a result.
+static int cu_count() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+template <int DH, int NW, int OCC>
+static hipError_t launch_flash_pad_nw(const AttnArgs<bf16>& a, hipStream_t st) {
+  constexpr int STAGES = 3;
   const long nwg = (long)cdiv(a.lq, NW * 32) * a.heads * a.n_streams;
   if (nwg * 64 * NW > 0xFFFFFFFFL) return hipErrorInvalidConfiguration;
-  if ((long)a.lk * a.k_ld * 2 > 0x7FFFFFFFL || (long)DH * a.vt_ld * 2 > 0x7FFFFFFFL)
-    return hipErrorInvalidValue;
-  // every 64-key tile of V^T must lie inside its padded row
-  if (a.vt_ld < round_up(a.lk, 64)) return hipErrorInvalidValue;
   if (a.kv_sel)
     hipLaunchKernelGGL((k_flash_pad<DH, NW, OCC, STAGES, true>), dim3((unsigned)nwg), dim3(64 * NW), 0,
                        st, a);
@@ -59,6 +74,21 @@ static hipError_t launch_flash_pad(const AttnArgs<bf16>& a, hipStream_t st) {
     hipLaunchKernelGGL((k_flash_pad<DH, NW, OCC, STAGES, false>), dim3((unsigned)nwg), dim3(64 * NW), 0,
                        st, a);
   return hipGetLastError();
+}
+
+template <int DH>
+static hipError_t launch_flash_pad(const AttnArgs<bf16>& a, hipStream_t st) {
+  if ((long)a.lk * a.k_ld * 2 > 0x7FFFFFFFL || (long)DH * a.vt_ld * 2 > 0x7FFFFFFFL)
+    return hipErrorInvalidValue;
+  // every 64-key tile of V^T must lie inside its padded row
+  if (a.vt_ld < round_up(a.lk, 64)) return hipErrorInvalidValue;
+  // estimated time in rounds of the CUs x queries per workgroup; eight waves
+  // run about 3.5% slower per query than twelve
+  const long cus = cu_count(), sh = (long)a.heads * a.n_streams;
+  const double t12 = (double)cdiv(cdiv(a.lq, 384) * sh, cus) * 384.0;
+  const double t8 = (double)cdiv(cdiv(a.lq, 256) * sh, cus) * 256.0 * 1.035;
+  if (t8 < t12) return launch_flash_pad_nw<DH, 8, 2>(a, st);
+  return launch_flash_pad_nw<DH, 12, 3>(a, st);
 }
 
 template <>
