@@ -541,7 +541,9 @@ CS_DEV void gemm_epilogue16_deep(const f32x4 (&acc)[TM][TN], int row_base, int c
 // accumulators between the register files.  The compiler does not see them
 // as matrix instructions, so the hazards it would otherwise cover are
 // covered here: the accumulators are written (bias) long before the first
-// product, and none is read until 24 wait states after the last product.
+// product, none is read until 24 wait states after the last product, and a
+// fragment register is rewritten by an LDS read no sooner than eight
+// products after the last product that used it.
 //
 // Same LDS row layout, tiled weights, tile order and accumulation order over
 // K as k_gemm_dl: results are bitwise equal to it.
