@@ -71,10 +71,13 @@ def test_velocity_tiny(dtype, init):
             assert err < TOL[dtype] / 4
 
 
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
 @pytest.mark.parametrize("init", ["paper", "stress"])
-def test_velocity_wan_mid_bf16(init):
-    say(f"velocity wan_mid bf16 init={init}")
-    gm, m = gpu_model("wan_mid", synth.DTYPE_BF16, init)
+def test_velocity_wan_mid(init, dtype):
+    """Wan2.1-1.3B widths (d = 1536, 12 x 128 heads, FFN 8960, 2 blocks, 384
+    tokens) in both arithmetic paths."""
+    say(f"velocity wan_mid dtype={dtype} init={init}")
+    gm, m = gpu_model("wan_mid", dtype, init)
     W = oracle_weights(m, init)
     x = synth.make_noise(m, 2, seed0=600)
     ctx = synth.make_context(m, 1)
@@ -84,7 +87,7 @@ def test_velocity_wan_mid_bf16(init):
     for i in range(2):
         err = rel_l2(v[i], odit.velocity(x[i], 0.7, emb, W, m))
         say(f"  i={i} rel_l2={err:.3e}")
-        assert err < TOL[0] / 2
+        assert err < TOL[dtype] / 2
 
 
 @pytest.mark.parametrize("name", ["wan5b_mid", "wan14b_mid"])
@@ -195,11 +198,14 @@ def test_rollout_tiny(dtype, n_branch):
         check_rollout(gm, wl, tau, dtype, okey=("tiny", n_branch))
 
 
-def test_rollout_wan_mid_bf16():
-    say("rollout wan_mid bf16 B=1 N=2")
+@pytest.mark.parametrize("n_branch", [1, 2])
+def test_rollout_wan_mid_bf16(n_branch):
+    """Wan2.1-1.3B widths (head dim 128, K = 1536 and 8960 projections):
+    conditional only, and with classifier-free guidance (two branches)."""
+    say(f"rollout wan_mid bf16 B={n_branch} N=2")
     gm, m = gpu_model("wan_mid", synth.DTYPE_BF16, "paper")
-    wl = synth.make_workload("wan_mid", n_branch=1, init="paper", n_cand=2)
-    g, res = check_rollout(gm, wl, 0.1, synth.DTYPE_BF16, okey=("wan_mid", 1))
+    wl = synth.make_workload("wan_mid", n_branch=n_branch, init="paper", n_cand=2)
+    g, res = check_rollout(gm, wl, 0.1, synth.DTYPE_BF16, okey=("wan_mid", n_branch))
     assert 0 < res.n_compute < res.n_calls
 
 
