@@ -198,6 +198,32 @@ def test_rollout_tiny(dtype, n_branch):
         check_rollout(gm, wl, tau, dtype, okey=("tiny", n_branch))
 
 
+A_RTOL = {synth.DTYPE_FP32: 1e-6, synth.DTYPE_BF16: 5e-3}   # measured: 6e-8 / 7.5e-4
+
+
+@pytest.mark.parametrize("n_branch", [1, 2])
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
+def test_indicator_values_match_oracle(dtype, n_branch):
+    """The accumulated drift statistic a (Eq. indicator) the decision kernel
+    reports at every step, on the oracle's schedule (replay, so both sides
+    follow the same trajectory): present on exactly the steps where the
+    oracle evaluates the rule, and equal to the oracle's value within the
+    latents' agreement (fp32 path: 1e-6 relative; bf16: 5e-3)."""
+    gm, m = gpu_model("tiny", dtype, "stress")
+    wl = workload("tiny", n_branch, "stress", dtype)
+    r = wl.roll
+    res = oracle_rollout(wl, 0.1, key=("tiny", n_branch))
+    om, oa = oracle_masks(res, r.n_cand, r.n_branch, r.n_steps)
+    g = run_rollout(gm, wl, tau=0.1, override=om)
+    assert np.array_equal(g.masks, om)
+    assert np.array_equal(np.isnan(g.a), np.isnan(oa))
+    both = ~np.isnan(oa)
+    assert both.sum() > 0
+    rel = np.abs(g.a[both] - oa[both]) / np.abs(oa[both])
+    say(f"indicator dtype={dtype} B={n_branch}: {both.sum()} values, max rel diff {rel.max():.3e}")
+    assert rel.max() < A_RTOL[dtype]
+
+
 @pytest.mark.parametrize("n_branch", [1, 2])
 def test_rollout_wan_mid_bf16(n_branch):
     """Wan2.1-1.3B widths (head dim 128, K = 1536 and 8960 projections):
