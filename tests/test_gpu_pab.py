@@ -73,9 +73,11 @@ def test_pab_rollout_tiny(dtype, n_branch):
     assert rel_l2(g.latents, off.latents) > 1e-5
 
 
-def test_pab_rollout_wan_mid_bf16():
-    say("PAB rollout wan_mid bf16 B=1 N=2, ranges 2 / 6")
-    wl = pab_workload("wan_mid", 1, synth.DTYPE_BF16, init="paper", n_cand=2, pab_self=2, pab_cross=6)
+@pytest.mark.parametrize("n_branch", [1, 2])
+def test_pab_rollout_wan_mid_bf16(n_branch):
+    say(f"PAB rollout wan_mid bf16 B={n_branch} N=2, ranges 2 / 6")
+    wl = pab_workload("wan_mid", n_branch, synth.DTYPE_BF16, init="paper", n_cand=2, pab_self=2,
+                      pab_cross=6)
     gm = GpuModel(wl.model, wl.weights)
     check_pab(gm, wl, synth.DTYPE_BF16)
 
