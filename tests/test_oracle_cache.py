@@ -157,3 +157,62 @@ def test_pruned_search_keeps_top_preview_and_matches_unpruned(tiny_b2):
     np.testing.assert_array_equal(res.latents, full.latents)   # preview does not perturb
     np.testing.assert_allclose(final, R.score(full.latents[kept], tiny_b2.scorer))
     assert winner in kept
+
+
+# ------------------------------------------------------------- exact tie
+def _exact_tie_run(fn=None):
+    """v(x) = -x on the grid 1, 3/4, 1/2, 1/4, 0 with x_1 = 1: every value
+    is a short dyadic fraction, so the indicator reaches tau = 1/4 exactly
+    at step 2 (x_2 = 5/4 x_1; ||x_2 - x_1|| / ||x_1|| = 1/4)."""
+    x1 = np.ones((1, 2, 4, 4))
+    run = fn or R.cached_rollout
+    return run(x1, [_neg], _grid(4), tau=0.25, k_warm=1, k_cool=1, guidance=1.0), x1
+
+
+def test_indicator_equal_to_tau_skips():
+    """Skip while a <= tau (Sec. Method, adaptive skip rule): at a = tau
+    exactly the call reuses Delta.  Hand-derived: computes at 1, 3, 4;
+    a = 1/4 at step 2 and 1/4 + 7/16 at step 3; x_5 = 2.24609375 x_1."""
+    res, x1 = _exact_tie_run()
+    assert res.schedule(0, 0) == [True, False, True, True]
+    assert res.a_values(0, 0) == [None, 0.25, 0.6875, None]
+    assert np.array_equal(res.latents, 2.24609375 * x1)
+
+
+# -------------------------------------------- planted mistakes are caught
+import inspect
+
+
+def _planted(old, new):
+    """A copy of the oracle's per-candidate rollout with one line changed."""
+    src = inspect.getsource(R.cached_rollout_one)
+    assert old in src, old
+    ns = dict(R.__dict__)
+    exec(compile(src.replace(old, new), "<planted>", "exec"), ns)
+    return ns["cached_rollout_one"]
+
+
+def _closed_form_holds():
+    try:
+        for case in json.load(open(os.path.join(GOLD, "cache_rule_closed_form.json")))["cases"]:
+            test_closed_form_cache_schedule(case)
+        test_indicator_equal_to_tau_skips()
+    except AssertionError:
+        return False
+    return True
+
+
+@pytest.mark.parametrize("old,new", [
+    ("compute = not (a[b] <= tau)", "compute = not (a[b] < tau)"),          # strictness
+    ("                a[b] = 0.0\n", ""),                                      # no reset after a compute
+    ("den = math.sqrt(float(np.sum(xref[b] ** 2)))",
+     "den = math.sqrt(float(np.sum(x ** 2)))"),                               # wrong normaliser
+    ("v[b] = x + delta[b]", "v[b] = x - delta[b]"),                          # sign of the reuse
+    ("x = x + (t_next - t_k) * vt", "x = x + (t_k - t_next) * vt"),          # Euler direction
+])
+def test_planted_rule_mistake_breaks_a_pin(monkeypatch, old, new):
+    """Each plausible slip in the cache rule or the update fails one of the
+    hand-derived pins above (the pins are not restatements of the code)."""
+    assert _closed_form_holds()
+    monkeypatch.setattr(R, "cached_rollout_one", _planted(old, new))
+    assert not _closed_form_holds()

@@ -79,3 +79,38 @@ def test_order_and_top1_and_regret():
     assert regret == pytest.approx(0.9 - 0.1)
     assert math.isnan(rank.spearman([1.0], [2.0]))
     assert math.isnan(rank.spearman([1.0, 1.0], [2.0, 3.0]))
+
+
+# -------------------------------------------- planted mistakes are caught
+import inspect
+
+
+def _planted(fn_name, old, new):
+    src = inspect.getsource(getattr(rank, fn_name))
+    assert old in src, old
+    ns = dict(rank.__dict__)
+    exec(compile(src.replace(old, new), "<planted>", "exec"), ns)
+    return ns[fn_name]
+
+
+def _pins_hold():
+    try:
+        test_spearman_with_ties_matches_scipy_and_counting()
+        test_order_and_top1_and_regret()
+        for n in (2, 3, 4):
+            test_spearman_matches_closed_form_all_permutations(n)
+    except AssertionError:
+        return False
+    return True
+
+
+@pytest.mark.parametrize("fn_name,old,new", [
+    ("average_ranks", "mean_rank = (pos + end) / 2.0 + 1.0", "mean_rank = pos + 1.0"),   # ordinal ties
+    ("order_desc", "key=lambda i: (-float(s[i]), i)", "key=lambda i: (float(s[i]), i)"),  # ascending
+    ("order_desc", "key=lambda i: (-float(s[i]), i)", "key=lambda i: (-float(s[i]), -i)"),  # tie order
+    ("pearson", "return sxy / math.sqrt(sxx * syy)", "return sxy / (sxx * syy)"),          # normaliser
+])
+def test_planted_rank_mistake_breaks_a_pin(monkeypatch, fn_name, old, new):
+    assert _pins_hold()
+    monkeypatch.setattr(rank, fn_name, _planted(fn_name, old, new))
+    assert not _pins_hold()
