@@ -164,6 +164,79 @@ hipError_t decide_finalize(const DecideParams& p, const double* partials, const 
   return hipGetLastError();
 }
 
+// One workgroup per (candidate, 1024 float4 of its latent): each thread
+// handles UPD_F4 float4 spaced a workgroup apart (coalesced) and issues all
+// of its loads before its stores.  The candidate and its branch masks are
+// uniform per workgroup.  FULL: every element of the thread is in range
+// (no per-element checks, so the loads are issued back to back).
+constexpr int UPD_F4 = 4;
+
+template <bool FULL>
+__device__ __forceinline__ void cache_update_body(float4* __restrict__ xp, float* __restrict__ xref,
+                                                  float* __restrict__ delta,
+                                                  const float* __restrict__ vbuf, const int (&m)[2],
+                                                  long s0, int n_branch, long D, long D4, long j0,
+                                                  float dt, float w, int store_state,
+                                                  float4* __restrict__ vtp) {
+  auto in = [&](int k) { return FULL || j0 + k * 256 < D4; };
+  float4 xv[UPD_F4], v[2][UPD_F4];
+#pragma unroll
+  for (int k = 0; k < UPD_F4; ++k)
+    if (in(k)) xv[k] = xp[j0 + k * 256];
+  // b runs to a compile-time bound so that v stays in registers
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    if (b >= n_branch) break;
+    const long s = s0 + b;
+    float4* dp = reinterpret_cast<float4*>(delta + s * D);
+    if (m[b]) {
+      const float4* vp = reinterpret_cast<const float4*>(vbuf + s * D);
+#pragma unroll
+      for (int k = 0; k < UPD_F4; ++k)
+        if (in(k)) v[b][k] = vp[j0 + k * 256];
+      if (store_state) {
+        float4* rp = reinterpret_cast<float4*>(xref + s * D);
+#pragma unroll
+        for (int k = 0; k < UPD_F4; ++k) {
+          if (!in(k)) continue;
+          float4 dv;
+          dv.x = v[b][k].x - xv[k].x; dv.y = v[b][k].y - xv[k].y;
+          dv.z = v[b][k].z - xv[k].z; dv.w = v[b][k].w - xv[k].w;
+          dp[j0 + k * 256] = dv;
+          rp[j0 + k * 256] = xv[k];
+        }
+      }
+    } else {
+      float4 dv[UPD_F4];
+#pragma unroll
+      for (int k = 0; k < UPD_F4; ++k)
+        if (in(k)) dv[k] = dp[j0 + k * 256];
+#pragma unroll
+      for (int k = 0; k < UPD_F4; ++k) {
+        if (!in(k)) continue;
+        v[b][k].x = xv[k].x + dv[k].x; v[b][k].y = xv[k].y + dv[k].y;
+        v[b][k].z = xv[k].z + dv[k].z; v[b][k].w = xv[k].w + dv[k].w;
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < UPD_F4; ++k) {
+    if (!in(k)) continue;
+    float4 vt = v[0][k];
+    if (n_branch == 2) {
+      vt.x = v[1][k].x + w * (v[0][k].x - v[1][k].x);
+      vt.y = v[1][k].y + w * (v[0][k].y - v[1][k].y);
+      vt.z = v[1][k].z + w * (v[0][k].z - v[1][k].z);
+      vt.w = v[1][k].w + w * (v[0][k].w - v[1][k].w);
+    }
+    float4 xn;
+    xn.x = xv[k].x + dt * vt.x; xn.y = xv[k].y + dt * vt.y;
+    xn.z = xv[k].z + dt * vt.z; xn.w = xv[k].w + dt * vt.w;
+    xp[j0 + k * 256] = xn;
+    if (vtp) vtp[j0 + k * 256] = vt;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_cache_update(float* __restrict__ x, float* __restrict__ xref,
                                                        float* __restrict__ delta,
                                                        const float* __restrict__ vbuf,
@@ -171,49 +244,26 @@ __global__ __launch_bounds__(256) void k_cache_update(float* __restrict__ x, flo
                                                        int n_branch, long D, float dt, float w,
                                                        int store_state, float* __restrict__ vt_out) {
   const long D4 = D >> 2;
-  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (long)n_cand * D4) return;
-  const int i = (int)(idx / D4);
-  const long j = idx - (long)i * D4;
-  float4* xp = reinterpret_cast<float4*>(x + (long)i * D) + j;
-  const float4 xv = *xp;
-  float4 v[2];
-  for (int b = 0; b < n_branch; ++b) {
-    const long s = (long)i * n_branch + b;
-    float4* dp = reinterpret_cast<float4*>(delta + s * D) + j;
-    if (mask[s]) {
-      const float4 vb = reinterpret_cast<const float4*>(vbuf + s * D)[j];
-      if (store_state) {
-        float4 dv;
-        dv.x = vb.x - xv.x; dv.y = vb.y - xv.y; dv.z = vb.z - xv.z; dv.w = vb.w - xv.w;
-        *dp = dv;
-        reinterpret_cast<float4*>(xref + s * D)[j] = xv;
-      }
-      v[b] = vb;
-    } else {
-      const float4 dv = *dp;
-      v[b].x = xv.x + dv.x; v[b].y = xv.y + dv.y; v[b].z = xv.z + dv.z; v[b].w = xv.w + dv.w;
-    }
-  }
-  float4 vt = v[0];
-  if (n_branch == 2) {
-    vt.x = v[1].x + w * (v[0].x - v[1].x);
-    vt.y = v[1].y + w * (v[0].y - v[1].y);
-    vt.z = v[1].z + w * (v[0].z - v[1].z);
-    vt.w = v[1].w + w * (v[0].w - v[1].w);
-  }
-  float4 xn;
-  xn.x = xv.x + dt * vt.x; xn.y = xv.y + dt * vt.y; xn.z = xv.z + dt * vt.z; xn.w = xv.w + dt * vt.w;
-  *xp = xn;
-  if (vt_out) reinterpret_cast<float4*>(vt_out + (long)i * D)[j] = vt;
+  const int i = blockIdx.y;
+  const long s0 = (long)i * n_branch;
+  const int m[2] = {mask[s0], n_branch == 2 ? (int)mask[s0 + 1] : 0};
+  const long j0 = (long)blockIdx.x * (256 * UPD_F4) + threadIdx.x;
+  float4* xp = reinterpret_cast<float4*>(x + (long)i * D);
+  float4* vtp = vt_out ? reinterpret_cast<float4*>(vt_out + (long)i * D) : nullptr;
+  if (j0 + (UPD_F4 - 1) * 256 < D4)
+    cache_update_body<true>(xp, xref, delta, vbuf, m, s0, n_branch, D, D4, j0, dt, w, store_state, vtp);
+  else
+    cache_update_body<false>(xp, xref, delta, vbuf, m, s0, n_branch, D, D4, j0, dt, w, store_state, vtp);
 }
 
 hipError_t cache_update(float* x, float* xref, float* delta, const float* vbuf, const uint8_t* mask,
                         int n_cand, int n_branch, long D, float dt, float guidance,
                         int store_state, float* vt_out, hipStream_t st) {
-  const long n = (long)n_cand * (D >> 2);
-  hipLaunchKernelGGL(k_cache_update, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, x, xref, delta,
-                     vbuf, mask, n_cand, n_branch, D, dt, guidance, store_state, vt_out);
+  if (n_cand <= 0 || D <= 0) return hipSuccess;
+  if (n_branch < 1 || n_branch > 2 || n_cand > 65535) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)cdiv(D >> 2, 256 * UPD_F4), (unsigned)n_cand);
+  hipLaunchKernelGGL(k_cache_update, grid, dim3(256), 0, st, x, xref, delta, vbuf, mask, n_cand, n_branch,
+                     D, dt, guidance, store_state, vt_out);
   return hipGetLastError();
 }
 
