@@ -281,7 +281,12 @@ def main():
                                  + (2 * computed if r.mode in (synth.CACHE_ADAPTIVE, synth.CACHE_STATIC) else 0)),
             "score": 8.0 * D * N * K,
         }
-        roof["streaming"] = {}
+        # each family's time is the sum of HIP-event brackets around its
+        # calls, so it includes every call's dispatch and event overhead:
+        # small against the 40 ms attention launches, but of the order of
+        # the 20-60 us these kernels take (rates below are lower bounds; a
+        # kernel trace gives the kernels alone)
+        roof["streaming"] = {"timing": "per-call HIP-event brackets incl. dispatch overhead (lower bound)"}
         for name, nbytes in stream_bytes.items():
             ms, n = fam[name]
             gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 and nbytes > 0 else None

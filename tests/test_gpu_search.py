@@ -151,15 +151,16 @@ def test_allocation_failure_is_reported_and_recoverable():
 
 @pytest.mark.parametrize("name,dtype,n_branch,n_cand",
                          [("tiny", synth.DTYPE_FP32, 2, 4), ("tiny", synth.DTYPE_BF16, 2, 4),
-                          ("wan_mid", synth.DTYPE_BF16, 1, 3)])
+                          ("ragged", synth.DTYPE_FP32, 2, 4), ("wan_mid", synth.DTYPE_BF16, 1, 3)])
 def test_pruned_search_matches_oracle(name, dtype, n_branch, n_cand):
     """Pruned composition: survivors, preview scores and winner agree with
     the oracle; survivors' latents equal the unpruned cached rollout's bit
-    for bit (retaining candidates does not perturb them).  Also at the
-    Wan2.1-1.3B widths."""
+    for bit (retaining candidates does not perturb them).  Also on the
+    ragged geometry (a latent that is not a whole number of update
+    workgroups) and at the Wan2.1-1.3B widths."""
     from paper_2607_23159_amd.search import pruned_search
     say(f"pruned search {name} dtype={dtype} B={n_branch} N={n_cand}")
-    init = "stress" if name == "tiny" else "paper"
+    init = "paper" if name == "wan_mid" else "stress"
     wl = synth.make_workload(name, n_branch=n_branch, init=init, dtype=dtype, n_cand=n_cand)
     gm = GpuModel(wl.model, wl.weights)
     res = pruned_search(gm, wl, prune_step=4, keep=2, mode="commit")
