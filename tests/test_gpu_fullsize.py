@@ -1,5 +1,6 @@
-"""GPU checks at the full Wan2.1-1.3B size in the launch configuration the
-bench times (8 streams of 32,760 tokens in one transformer call).
+"""GPU checks at full size in the launch configurations the bench times
+(Wan2.1-1.3B: 8 streams of 32,760 tokens in one transformer call; one
+Wan2.2-5B block: 4 streams of 27,280 tokens).
 
 The oracle cannot run whole full-size rollouts, so they are checked on
 sampled outputs it computes one by one (one block, sampled tokens) and
@@ -37,33 +38,52 @@ def _gpu():
     B.lib()
 
 
+def _block_sampled(m, n, rows, sampled, single):
+    """One block on n full-length latents in one call: sampled tokens of the
+    streams in `sampled` against the oracle, the streams in `single` bitwise
+    equal to their own single-stream calls."""
+    w = synth.make_weights(m, init="stress")
+    gm = GpuModel(m, w)
+    W = {k: v.astype(np.float64) for k, v in synth.unflatten(m, w).items()}
+    x = synth.make_noise(m, n, seed0=900)
+    ctx = synth.make_context(m, 1)
+    xd = torch.from_numpy(x.reshape(n, -1)).cuda()
+    cd = torch.from_numpy(ctx).cuda()
+    vn = gm.velocity(xd, 0.6, cd)
+    emb = odit.text_embedding(ctx, W)
+    for i in sampled:
+        vp = odit.patchify(vn[i].cpu().numpy().reshape(x.shape[1:]), m.patch_t, m.patch_h, m.patch_w)
+        ref = odit.velocity(x[i], 0.6, emb, W, m, last_block_rows=rows)
+        err = rel_l2(vp[rows], ref)
+        say(f"  stream {i} sampled rel_l2={err:.3e}")
+        assert err < TOL[0] / 2
+    for i in single:
+        one = gm.velocity(xd[i:i + 1].contiguous(), 0.6, cd)
+        assert torch.equal(one[0], vn[i])
+    gm.close()
+
+
 def test_block_8_streams_full_length_sampled():
     """One Wan2.1-1.3B block, 8 latents of 32,760 tokens in one call (the
     bench's row count, 262,080 GEMM rows): sampled tokens of two streams
     against the oracle, and every stream bitwise equal to its own
     single-stream call."""
     say("one block, 8 streams x 32760 tokens, bf16")
-    m = synth.MODELS["wan13b_block1"]
-    w = synth.make_weights(m, init="stress")
-    gm = GpuModel(m, w)
-    W = {k: v.astype(np.float64) for k, v in synth.unflatten(m, w).items()}
-    x = synth.make_noise(m, 8, seed0=900)
-    ctx = synth.make_context(m, 1)
-    xd = torch.from_numpy(x.reshape(8, -1)).cuda()
-    cd = torch.from_numpy(ctx).cuda()
-    v8 = gm.velocity(xd, 0.6, cd)
-    emb = odit.text_embedding(ctx, W)
-    rows = np.array([0, 255, 256, 16384, 32511, 32759])
-    for i in (0, 7):
-        vp = odit.patchify(v8[i].cpu().numpy().reshape(x.shape[1:]), 1, 2, 2)
-        ref = odit.velocity(x[i], 0.6, emb, W, m, last_block_rows=rows)
-        err = rel_l2(vp[rows], ref)
-        say(f"  stream {i} sampled rel_l2={err:.3e}")
-        assert err < TOL[0] / 2
-    for i in (0, 3, 7):
-        one = gm.velocity(xd[i:i + 1].contiguous(), 0.6, cd)
-        assert torch.equal(one[0], v8[i])
-    gm.close()
+    _block_sampled(synth.MODELS["wan13b_block1"], 8, np.array([0, 255, 256, 16384, 32511, 32759]),
+                   (0, 7), (0, 3, 7))
+
+
+def test_block_wan5b_4_streams_full_length_sampled():
+    """One Wan2.2-5B block (d = 3072, 24 heads, FFN 14336), 4 latents of
+    27,280 tokens in one call, the 5B workload's launch shape: 71 full
+    query tiles of 384 and a 16-query last one per head, 426 full key tiles
+    of 64 and a 16-key last one.  Sampled tokens across those boundaries
+    against the oracle; streams bitwise equal to single-stream calls."""
+    say("one Wan2.2-5B block, 4 streams x 27280 tokens, bf16")
+    m = dataclasses.replace(synth.MODELS["wan5b"], n_blocks=1)
+    L = (m.lat_f // m.patch_t) * (m.lat_h // m.patch_h) * (m.lat_w // m.patch_w)
+    assert L == 27280
+    _block_sampled(m, 4, np.array([0, 383, 384, 13640, 27263, 27264, L - 1]), (0, 3), (0, 3))
 
 
 @pytest.fixture(scope="module")
