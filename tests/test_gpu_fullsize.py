@@ -1,6 +1,7 @@
 """GPU checks at full size in the launch configurations the bench times
 (Wan2.1-1.3B: 8 streams of 32,760 tokens in one transformer call; one
-Wan2.2-5B block: 4 streams of 27,280 tokens).
+Wan2.2-5B block: 4 streams of 27,280 tokens; one Wan2.1-14B block: 4
+streams of 32,760 tokens).
 
 The oracle cannot run whole full-size rollouts, so they are checked on
 sampled outputs it computes one by one (one block, sampled tokens) and
@@ -84,6 +85,17 @@ def test_block_wan5b_4_streams_full_length_sampled():
     L = (m.lat_f // m.patch_t) * (m.lat_h // m.patch_h) * (m.lat_w // m.patch_w)
     assert L == 27280
     _block_sampled(m, 4, np.array([0, 383, 384, 13640, 27263, 27264, L - 1]), (0, 3), (0, 3))
+
+
+def test_block_wan14b_4_streams_full_length_sampled():
+    """One Wan2.1-14B block (d = 5120, 40 heads, FFN 13824), 4 latents of
+    32,760 tokens in one call, the 14B workload's launch shape: every
+    residual projection (K = 5120 and 13824) runs on the one-wave-per-SIMD
+    GEMM with the deep residual epilogue.  Sampled tokens of one stream
+    against the oracle; streams bitwise equal to single-stream calls."""
+    say("one Wan2.1-14B block, 4 streams x 32760 tokens, bf16")
+    m = dataclasses.replace(synth.MODELS["wan14b"], n_blocks=1)
+    _block_sampled(m, 4, np.array([0, 383, 384, 16384, 32639, 32640, 32759]), (3,), (0, 3))
 
 
 @pytest.fixture(scope="module")
