@@ -74,6 +74,17 @@ def test_block_8_streams_full_length_sampled():
                    (0, 7), (0, 3, 7))
 
 
+def test_block_16_streams_full_length_sampled():
+    """One Wan2.1-1.3B block, 16 latents of 32,760 tokens in one call, the
+    launch shape of a guided (two-branch) rollout of 8 seeds: 524,160 GEMM
+    rows, an FFN hidden activation of 4.7e9 elements (offsets past 2^32).
+    Sampled tokens of the first and last stream against the oracle; the last
+    stream bitwise equal to its single-stream call."""
+    say("one block, 16 streams x 32760 tokens, bf16")
+    _block_sampled(synth.MODELS["wan13b_block1"], 16, np.array([0, 255, 256, 16384, 32511, 32759]),
+                   (0, 15), (15,))
+
+
 def test_block_wan5b_4_streams_full_length_sampled():
     """One Wan2.2-5B block (d = 3072, 24 heads, FFN 14336), 4 latents of
     27,280 tokens in one call, the 5B workload's launch shape: 71 full
