@@ -118,10 +118,13 @@ def full_model():
     gm.close()
 
 
-def _short(m, w, n_cand, seed0=100, **kw):
-    roll = synth.RolloutCfg(n_cand=n_cand, n_steps=4, k_warm=1, k_cool=1, **kw)
+def _short(m, w, n_cand, seed0=100, n_branch=1, **kw):
+    roll = synth.RolloutCfg(n_cand=n_cand, n_steps=4, k_warm=1, k_cool=1, n_branch=n_branch, **kw)
+    ctx = [synth.make_context(m, synth.CTX_COND_SEED)]
+    if n_branch == 2:
+        ctx.append(synth.make_context(m, synth.CTX_UNCOND_SEED))
     return synth.Workload(name="wan13b_short", model=m, roll=roll, weights=w,
-                          ctx=[synth.make_context(m, synth.CTX_COND_SEED)],
+                          ctx=ctx,
                           noise=synth.make_noise(m, n_cand, seed0=seed0),
                           scorer=synth.make_scorer(m), timesteps=synth.timestep_grid(4))
 
@@ -147,4 +150,28 @@ def test_full_model_rollout_properties(full_model):
     s = run_rollout(gm, one, tau=0.1)
     t = run_rollout(gm, wl, tau=0.1)
     assert np.array_equal(s.masks[:, 0], t.masks[:, 1])
+    assert np.array_equal(s.latents[0], t.latents[1])
+
+
+def test_full_model_guided_rollout_properties(full_model):
+    """Full 30-block model with guidance (B = 2, w = 5), 2 seeds, 4 steps:
+    tau = 0 reproduces the uncached guided rollout bit for bit, tau = inf
+    computes only the forced windows and both branches decide alike (they
+    see the same latent), and a seed's guided rollout is the same alone and
+    in a batch."""
+    m, w, gm = full_model
+    wl = _short(m, w, 2, n_branch=2)
+    say("full model, B=2: tau=0 vs off")
+    a = run_rollout(gm, wl, tau=0.0)
+    b = run_rollout(gm, wl, mode=synth.CACHE_OFF)
+    assert a.computed == a.calls == 2 * 2 * 4
+    assert np.array_equal(a.latents, b.latents) and np.array_equal(a.scores, b.scores)
+    say("full model, B=2: tau=inf forced only")
+    c = run_rollout(gm, wl, tau=math.inf)
+    assert c.masks.shape == (4, 4) and (c.masks.sum(axis=0) == 2).all()
+    assert np.array_equal(c.masks[:, 0::2], c.masks[:, 1::2])
+    say("full model, B=2: seed 101 alone vs in the batch")
+    one = _short(m, w, 1, seed0=101, n_branch=2)
+    s = run_rollout(gm, one, tau=0.1)
+    t = run_rollout(gm, wl, tau=0.1)
     assert np.array_equal(s.latents[0], t.latents[1])
