@@ -1,25 +1,44 @@
 """Benchmark: cached candidate denoise-steps/s on one MI355X.
 
-One step = one CachedSearch exploration pass (Alg. 1) over one batch of
-synthetic inputs: rollout init (cache reset, text keys/values), T Euler
-steps of N candidates with the cache decision, transformer on the computed
-calls, skip/refresh/CFG/Euler update, then scoring and ranking.  The
-full-compute reference rollout of the same seeds (cache off) is tau
-independent; with --reference it is run once before the timed region and
-the cached ranking is compared with it (Spearman rho, top-1).
+Units.  One bench step is one denoise step of the N-candidate batch: the
+cache decision for every candidate and guidance branch, the transformer on
+the computing calls, the fused skip/refresh/CFG/Euler update (Alg. 1, one
+iteration of the step loop).  ``--warmup W`` runs W such steps untimed (a
+partial rollout, then discarded).  ``--steps K`` asks for K timed steps; the
+bench times whole cached rollouts, ceil(K / T) of them, so the timed region
+always holds complete decision schedules (forced warmup and cooldown windows
+included, not only the skip-rich middle), plus rollout init, scoring and
+ranking.  ``steps`` in the output is the number of denoise steps actually
+timed (a multiple of T) and ``ms_per_step`` is per denoise step;
+``value`` = N x timed steps / wall time.
+
+Legs after the headline, each run only if its estimated time fits the
+remaining wall-clock budget (``--budget-s`` from process start; a leg that
+does not fit is reported as skipped, never started):
+  * the CPU oracle on a bounded sample of the workload (cpu_baseline);
+  * the full (uncached) reference rollout of the same seeds, for Spearman
+    rho, top-1 agreement, regret and the cost model (Sec. Method, cost
+    analysis: C_c, C_f, gamma, break-even N);
+  * one guided rollout (B = 2, w = 5, both branches evaluated per step);
+  * the tau sweep, one cached rollout per extra tau, ranked against the
+    same reference.
 
 Printed: one JSON line with the metric, the roofline of the dominant kernel
 (self-attention, timed by HIP events on the rollout stream inside the
-library), and the CPU oracle timed on a bounded sample of the same workload.
+library), the GEMM family's rate, the streaming kernels' HBM rates, and the
+CPU oracle's rate.
 """
 from __future__ import annotations
 
 import argparse
+import collections
 import json
 import math
 import os
 import sys
 import time
+
+T_START = time.monotonic()
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -30,6 +49,7 @@ PEAK_HBM_GBS = 8000.0
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "self_attention_traffic_wan13b_n8_tau0.1.md")
 ATTN_SOURCES = [os.path.join(ROOT, "paper_2607_23159_amd", "csrc", f)
                 for f in ("attn_kernel.hpp", "k_attn.hip", "common.hpp")]
+DEFAULT_BUDGET_S = 480.0
 
 
 def attn_source_hash() -> str:
@@ -60,30 +80,100 @@ def measured_traffic(workload: str, n_branch: int):
         return None
 
 
-def parse():
+# ------------------------------------------------------------ host logic
+def timed_rollouts(steps: int, n_steps: int) -> int:
+    """Whole rollouts timed for a request of ``steps`` denoise steps."""
+    if steps < 1 or n_steps < 1:
+        raise ValueError("steps and n_steps must be >= 1")
+    return -(-steps // n_steps)
+
+
+class Budget:
+    """Wall-clock budget from process start; a leg starts only if its
+    estimate fits what is left."""
+
+    def __init__(self, limit_s: float, start: float = T_START, clock=time.monotonic):
+        self.limit, self.start, self.clock = float(limit_s), start, clock
+
+    def elapsed(self) -> float:
+        return self.clock() - self.start
+
+    def left(self) -> float:
+        return self.limit - self.elapsed()
+
+    def fits(self, estimate_s: float) -> bool:
+        return estimate_s <= self.left()
+
+
+def leg_estimates(rollout_s: float, computed: int, n_cand: int, n_steps: int, n_branch: int):
+    """Conservative time estimates (s) of the optional legs from one timed
+    cached rollout: rollout_s wall seconds in which ``computed`` of the
+    n_cand * n_branch * n_steps transformer calls ran."""
+    calls = n_cand * n_branch * n_steps
+    per_eval = rollout_s / max(computed, 1)
+    full = per_eval * calls * 1.05
+    return {
+        "reference": full,
+        # a guided rollout evaluates both branches; its skip fraction is
+        # close to the unguided one, allow 15% more
+        "cfg": rollout_s * (2.0 if n_branch == 1 else 1.0) * 1.15,
+        # a smaller tau computes more: bounded by the full rollout
+        "sweep_lower": min(full, rollout_s * 1.35),
+        "sweep_higher": rollout_s * 1.05,
+    }
+
+
+def n_compute_histogram(masks) -> dict:
+    """{computing streams in a step: number of steps} over [T][S] masks."""
+    c = collections.Counter(int(sum(int(v) for v in row)) for row in masks)
+    return {str(k): c[k] for k in sorted(c)}
+
+
+def cpu_model_name() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def parse(argv=None):
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=1)
-    p.add_argument("--warmup", type=int, default=0)
+    p.add_argument("--steps", type=int, default=50,
+                   help="timed denoise steps requested (rounded up to whole rollouts)")
+    p.add_argument("--warmup", type=int, default=5, help="untimed denoise steps")
     p.add_argument("--workload", default="wan13b_cached")
     p.add_argument("--tau", type=float, default=None)
     p.add_argument("--n-cand", type=int, default=None)
     p.add_argument("--n-steps", type=int, default=None)
-    p.add_argument("--cfg", action="store_true", help="two guidance branches (w = 5.0)")
+    p.add_argument("--cfg", action="store_true", help="two guidance branches (w = 5.0) in the headline")
     p.add_argument("--fp32", action="store_true", help="fp32 transformer arithmetic")
-    p.add_argument("--reference", action="store_true", help="also run the full rollouts for rho")
-    p.add_argument("--tau-sweep", default="", help="comma-separated extra tau values, one rollout each")
+    p.add_argument("--reference", choices=["auto", "on", "off"], default="auto",
+                   help="full-rollout reference for rho (auto: when N >= 2 and it fits the budget)")
+    p.add_argument("--no-cfg-leg", action="store_true", help="skip the guided (B = 2) rollout leg")
+    p.add_argument("--tau-sweep", default=None,
+                   help="comma-separated extra tau values (default 0.05,0.2 in adaptive mode)")
+    p.add_argument("--budget-s", type=float, default=DEFAULT_BUDGET_S,
+                   help="wall-clock budget from process start for all legs")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true", help="no per-kernel HIP event timing")
     p.add_argument("--mode", choices=["adaptive", "static", "pab"], default="adaptive",
                    help="reuse engine: the drift-indicator cache, the static schedule, or "
                         "attention-output broadcasting")
+    p.add_argument("--static-k", type=int, default=None, help="static schedule period")
     p.add_argument("--pab-self", type=int, default=2, help="self-attention broadcast range")
     p.add_argument("--pab-cross", type=int, default=6, help="cross-attention broadcast range")
     p.add_argument("--calibration-copy", type=int, default=0,
                    help="bytes of one plain device-to-device copy made before timing (a "
                         "known-size reference for HBM counter runs)")
-    return p.parse_args()
+    a = p.parse_args(argv)
+    if a.steps < 1 or a.warmup < 0:
+        p.error("--steps must be >= 1 and --warmup >= 0")
+    return a
 
 
 def cpu_baseline(model_cfg, computed_per_cand_step: float, n_branch: int):
@@ -122,7 +212,7 @@ def cpu_baseline(model_cfg, computed_per_cand_step: float, n_branch: int):
     eval_s = block_s * model_cfg.n_blocks
     cand_step_s = eval_s * computed_per_cand_step
     return {"value": 1.0 / cand_step_s, "unit": "candidate-steps/s", "cores": int(cores),
-            "kind": "oracle",
+            "cpu_model": cpu_model_name(), "kind": "oracle",
             "sample": (f"float64 oracle, one {model_cfg.hidden}-wide block at {L} tokens with {R1} and {R2} "
                        f"sampled query rows ({times[R1]:.1f} s, {times[R2]:.1f} s), extrapolated to all "
                        f"rows x {model_cfg.n_blocks} blocks = {eval_s:.0f} s per transformer call, "
@@ -131,16 +221,45 @@ def cpu_baseline(model_cfg, computed_per_cand_step: float, n_branch: int):
 
 
 def progress(msg: str) -> None:
-    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+    print(f"[bench {time.strftime('%H:%M:%S')} +{time.monotonic() - T_START:.0f}s] {msg}",
+          file=sys.stderr, flush=True)
 
 
-def main():
-    args = parse()
+def kernel_rates(fam, m, evals, self_evals, cross_evals, fp32):
+    """Self-attention roofline and GEMM family rate from per-family HIP-event
+    totals over ``evals`` stream evaluations."""
+    L, d = m.tokens, m.hidden
+    sa_ms, sa_n = fam["self_attn"]
+    flops = 4.0 * L * L * d * m.n_blocks * self_evals   # QK^T and PV, 2 flop per MAC
+    ach = flops / (sa_ms * 1e-3) / 1e12 if sa_ms > 0 else 0.0
+    peak = PEAK_FP32_TFLOPS if fp32 else PEAK_BF16_TFLOPS
+    g_ms, _ = fam["gemm"]
+    # QKV + out-projection (4 d^2) on self-attention evaluations, cross q +
+    # out-projection (2 d^2) on cross-attention evaluations, FFN (2 d F),
+    # patch embedding and head on every evaluation
+    gflops = (2.0 * L * m.n_blocks * (4 * d * d * self_evals + 2 * d * d * cross_evals
+                                      + 2 * d * m.ffn * evals)
+              + 4.0 * L * d * m.patch_dim * evals)
+    g_ach = gflops / (g_ms * 1e-3) / 1e12 if g_ms > 0 else None
+    return {"self_attn": {"achieved": round(ach, 1), "frac": round(ach / peak, 4),
+                          "launches": sa_n, "avg_launch_ms": round(sa_ms / max(sa_n, 1), 3),
+                          "flop_per_launch": flops / max(sa_n, 1)},
+            "gemm": {"achieved": None if g_ach is None else round(g_ach, 1),
+                     "frac": None if g_ach is None else round(g_ach / peak, 4)},
+            "peak": peak,
+            "family_ms": {k: round(v[0], 2) for k, v in fam.items()}}
+
+
+def main(argv=None):
+    args = parse(argv)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(candidates would shard across GPUs with no per-step traffic); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
+    budget = Budget(args.budget_s)
+
+    import dataclasses
 
     import numpy as np
     import torch
@@ -151,15 +270,21 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     B.lib()
+    progress("torch and the library loaded")
     dtype = synth.DTYPE_FP32 if args.fp32 else synth.DTYPE_BF16
     nb = 2 if args.cfg else 1
     t_gen = time.perf_counter()
     mode = {"adaptive": synth.CACHE_ADAPTIVE, "static": synth.CACHE_STATIC,
             "pab": synth.CACHE_PAB}[args.mode]
-    wl = synth.make_workload(args.workload, n_branch=nb, dtype=dtype, n_cand=args.n_cand,
-                             n_steps=args.n_steps, tau=args.tau, mode=mode,
-                             pab_self=args.pab_self, pab_cross=args.pab_cross)
-    m, r = wl.model, wl.roll
+    extra = {} if args.static_k is None else {"static_k": args.static_k}
+    # the guided leg needs the unconditional context: draw it whenever that
+    # leg may run (the headline's own inputs do not change)
+    want_cfg_leg = nb == 1 and not args.no_cfg_leg
+    wl = synth.make_workload(args.workload, n_branch=2 if want_cfg_leg else nb, dtype=dtype,
+                             n_cand=args.n_cand, n_steps=args.n_steps, tau=args.tau, mode=mode,
+                             pab_self=args.pab_self, pab_cross=args.pab_cross, **extra)
+    m = wl.model
+    r = dataclasses.replace(wl.roll, n_branch=nb)
     gen_s = time.perf_counter() - t_gen
     progress(f"inputs generated ({gen_s:.1f} s); uploading weights")
     gm = GpuModel(m, wl.weights)
@@ -168,24 +293,31 @@ def main():
     wl.weights = None
     N, T = r.n_cand, r.n_steps
     S = N * nb
+    R = timed_rollouts(args.steps, T)
 
-    reused = [0, 0]   # self / cross attention reuses, accumulated by rollout()
-
-    def rollout(mode=None, label="cached"):
-        desc = B.RolloutDesc(r, wl.timesteps, **({} if mode is None else {"mode": mode}))
-        h = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[1] if nb == 2 else None)
+    def rollout(roll, label, record=None, counters=None):
+        """One rollout of ``roll``; returns (scores, computed, calls, seconds)."""
+        desc = B.RolloutDesc(roll, wl.timesteps)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        h = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[1] if roll.n_branch == 2 else None)
         try:
-            for k in range(1, T + 1):
+            for k in range(1, roll.n_steps + 1):
+                if record is not None:
+                    mk, _ = B.cs_cache_decide(h, k, roll.n_cand * roll.n_branch)
+                    record.append(mk.copy())
                 B.cs_denoise_step(h, k)
                 if k % 10 == 0:
-                    progress(f"{label} rollout: step {k}/{T}")
-            scores = B.cs_score(h, inp.w, N)
+                    progress(f"{label} rollout: step {k}/{roll.n_steps}")
+            scores = B.cs_score(h, inp.w, roll.n_cand)
             st = B.cs_rollout_stats(h)
-            reused[0] += int(st.self_reused)
-            reused[1] += int(st.cross_reused)
-            return scores, int(st.computed), int(st.calls)
+            if counters is not None:
+                counters[0] += int(st.self_reused)
+                counters[1] += int(st.cross_reused)
         finally:
             B.cs_rollout_free(h)
+        torch.cuda.synchronize()
+        return scores, int(st.computed), int(st.calls), time.perf_counter() - t0
 
     if args.calibration_copy > 0:
         src = torch.empty(args.calibration_copy, dtype=torch.uint8, device="cuda")
@@ -199,72 +331,63 @@ def main():
     v = torch.empty_like(inp.x1[:1])
     B.cs_velocity(gm.h, inp.x1[:1], 1, 1.0, inp.ctx[0], v)
     torch.cuda.synchronize()
+    del v
 
-    ref_scores = None
-    full_s = None
-    if args.reference:
+    # warmup: W untimed denoise steps of the timed workload (partial rollout)
+    if args.warmup > 0:
+        h = B.cs_rollout_init(gm.h, B.RolloutDesc(r, wl.timesteps), inp.x1, inp.ctx[0],
+                              inp.ctx[1] if nb == 2 else None)
+        try:
+            for k in range(1, min(args.warmup, T) + 1):
+                B.cs_denoise_step(h, k)
+        finally:
+            B.cs_rollout_free(h)
         torch.cuda.synchronize()
-        t_ref = time.perf_counter()
-        ref_scores, _, _ = rollout(mode=synth.CACHE_OFF, label="full reference")
-        full_s = time.perf_counter() - t_ref
+        progress(f"{min(args.warmup, T)} warmup steps done")
 
-    for _ in range(args.warmup):
-        rollout(label="warmup")
-    torch.cuda.synchronize()
-
+    # ---- headline: R whole cached rollouts, timed
     if not args.no_profile:
         B.cs_profile_enable(gm.h, True)
         B.cs_profile_reset(gm.h)
     computed = calls = 0
-    rho = top1 = None
-    reused[0] = reused[1] = 0
+    reused = [0, 0]
+    masks = []
+    scores = None
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        scores, c, n = rollout(label="timed")
+    done = 0
+    for i in range(R):
+        scores, c, n, _ = rollout(r, f"timed {i + 1}/{R}", record=masks, counters=reused)
         computed += c
         calls += n
-        if N < 2:
-            pass                     # one candidate: nothing to rank (cs_rank needs n >= 2)
-        elif ref_scores is not None:
-            _, _, rho, top1 = B.cs_rank(scores, ref_scores)
-        else:
-            B.cs_rank(scores, scores)
+        done += 1
+        B.cs_rank(scores, None)                # the ranking step of the pass
+        if i + 1 < R and not budget.fits((time.perf_counter() - t0) / done * 1.1):
+            progress(f"budget: stopping after {done} of {R} timed rollouts")
+            break
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
-    value = N * T * args.steps / wall
+    steps_timed = done * T
+    ms_per_step = wall * 1e3 / steps_timed
+    value = N * steps_timed / wall
+    rollout_s = wall / done
+    progress(f"headline: {value:.3f} candidate-steps/s ({rollout_s:.1f} s per rollout)")
 
+    roof = None
     fam = {}
     if not args.no_profile:
         for f, name in enumerate(B.KERNEL_FAMILIES):
             fam[name] = B.cs_profile_read(gm.h, f)
-        B.cs_profile_enable(gm.h, False)
-
-    L, d = m.tokens, m.hidden
-    evals = computed                                   # stream evaluations in the timed region
-    self_evals = computed - reused[0]                  # of which ran self-attention
-    cross_evals = computed - reused[1]                 # ... and cross-attention
-    roof = None
     if fam:
-        sa_ms, sa_n = fam["self_attn"]
-        flops = 4.0 * L * L * d * m.n_blocks * self_evals   # QK^T and PV, 2 flop per MAC
-        ach = flops / (sa_ms * 1e-3) / 1e12 if sa_ms > 0 else 0.0
-        peak = PEAK_FP32_TFLOPS if args.fp32 else PEAK_BF16_TFLOPS
-        roof = {"bound": "mfma", "kernel": "k_flash (self-attention)", "achieved": round(ach, 1),
-                "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+        kr = kernel_rates(fam, m, computed, computed - reused[0], computed - reused[1], args.fp32)
+        sa = kr["self_attn"]
+        roof = {"bound": "mfma", "kernel": "k_flash_pad (self-attention)", "achieved": sa["achieved"],
+                "peak": kr["peak"], "unit": "TFLOP/s", "frac": sa["frac"],
                 "traffic": measured_traffic(args.workload, nb) if not args.fp32 else None,
-                "launches": sa_n, "avg_launch_ms": round(sa_ms / max(sa_n, 1), 3),
-                "flop_per_launch": flops / max(sa_n, 1)}
-        g_ms, g_n = fam["gemm"]
-        F = m.ffn
-        # QKV + out-projection (4 d^2) on self-attention evaluations, cross q +
-        # out-projection (2 d^2) on cross-attention evaluations, FFN (2 d F),
-        # patch embedding and head on every evaluation
-        gflops = (2.0 * L * m.n_blocks * (4 * d * d * self_evals + 2 * d * d * cross_evals + 2 * d * F * evals)
-                  + 4.0 * L * d * m.patch_dim * evals)
-        roof["gemm_tflops"] = round(gflops / (g_ms * 1e-3) / 1e12, 1) if g_ms > 0 else None
-        roof["family_ms"] = {k: round(vv[0], 2) for k, vv in fam.items()}
+                "launches": sa["launches"], "avg_launch_ms": sa["avg_launch_ms"],
+                "flop_per_launch": sa["flop_per_launch"],
+                "gemm_tflops": kr["gemm"]["achieved"], "gemm_frac": kr["gemm"]["frac"],
+                "family_ms": kr["family_ms"]}
         # streaming kernels against the HBM roofline, algorithmic bytes:
         # decision reads x and every branch's x_ref on each step past the
         # forced windows; the fused update reads and writes x, reads v (or
@@ -272,14 +395,13 @@ def main():
         # writes Delta, x_ref per computed stream; scoring reads x and w per
         # candidate
         D = int(np.prod(wl.noise.shape[1:]))
-        K = args.steps
         adaptive = r.mode == synth.CACHE_ADAPTIVE
-        dec_launches = (T - r.k_warm - r.k_cool) * K if adaptive else 0
+        dec_launches = (T - r.k_warm - r.k_cool) * done if adaptive else 0
         stream_bytes = {
             "decide": 4.0 * D * N * (1 + nb) * dec_launches,
-            "update": 4.0 * D * (2 * N * T * K + S * T * K
+            "update": 4.0 * D * (2 * N * T * done + S * T * done
                                  + (2 * computed if r.mode in (synth.CACHE_ADAPTIVE, synth.CACHE_STATIC) else 0)),
-            "score": 8.0 * D * N * K,
+            "score": 8.0 * D * N * done,
         }
         # each family's time is the sum of HIP-event brackets around its
         # calls, so it includes every call's dispatch and event overhead:
@@ -294,38 +416,53 @@ def main():
                                        "GB/s": None if gbs is None else round(gbs, 1),
                                        "frac": None if gbs is None else round(gbs / PEAK_HBM_GBS, 4)}
 
-    # tau sweep (each value: one timed cached rollout, compared with the
-    # reference when it was run)
-    sweep = []
-    for tv in [float(x) for x in args.tau_sweep.split(",") if x.strip()]:
-        r_t = __import__("dataclasses").replace(r, tau=tv)
-        desc = B.RolloutDesc(r_t, wl.timesteps)
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        h = B.cs_rollout_init(gm.h, desc, inp.x1, inp.ctx[0], inp.ctx[1] if nb == 2 else None)
-        try:
-            for k in range(1, T + 1):
-                B.cs_denoise_step(h, k)
-                if k % 10 == 0:
-                    progress(f"tau={tv} rollout: step {k}/{T}")
-            sc = B.cs_score(h, inp.w, N)
-            st = B.cs_rollout_stats(h)
-        finally:
-            B.cs_rollout_free(h)
-        dt_s = time.perf_counter() - t1
-        rec = {"tau": tv, "candidate_steps_per_s": round(N * T / dt_s, 4),
-               "skip_fraction": round(1 - st.computed / st.calls, 4), "ms_per_rollout": round(dt_s * 1e3, 1)}
-        if ref_scores is not None and N >= 2:
-            _, _, rho_t, top1_t = B.cs_rank(sc, ref_scores)
-            rec.update({"rho_vs_full": rho_t, "top1_vs_full": top1_t,
-                        "regret": float(max(ref_scores) - ref_scores[int(np.argmax(sc))])})
-        sweep.append(rec)
+    skipped = {}
+    est = leg_estimates(rollout_s, computed // done, N, T, nb)
 
-    # cost model (Sec. Method, cost analysis): per-rollout costs of the
-    # cached (C_c) and full (C_f) N-candidate batches, per candidate
+    # ---- CPU oracle on a bounded sample (about 10 s of host work)
+    cpu = None
+    if not args.no_cpu_baseline:
+        if budget.fits(60.0):
+            progress("timing the CPU oracle on a sample")
+            try:
+                cpu = cpu_baseline(m, computed / (N * steps_timed), nb)
+            except Exception as e:  # report, never hide
+                cpu = {"value": None, "error": repr(e)}
+        else:
+            skipped["cpu_baseline"] = "wall-clock budget"
+
+    def profiled_leg(roll, label, record=None):
+        if not args.no_profile:
+            B.cs_profile_reset(gm.h)
+        cnt = [0, 0]
+        out = rollout(roll, label, record=record, counters=cnt)
+        rates = None
+        if not args.no_profile:
+            f2 = {name: B.cs_profile_read(gm.h, f) for f, name in enumerate(B.KERNEL_FAMILIES)}
+            c = out[1]
+            kr2 = kernel_rates(f2, m, c, c - cnt[0], c - cnt[1], args.fp32)
+            rates = {"self_attn_frac": kr2["self_attn"]["frac"],
+                     "self_attn_tflops": kr2["self_attn"]["achieved"],
+                     "gemm_tflops": kr2["gemm"]["achieved"], "gemm_frac": kr2["gemm"]["frac"]}
+        return out, rates
+
+    # ---- full reference (cache off, same seeds): rho, top-1, costs
+    ref_scores = full_s = None
+    rho = top1 = regret = None
+    want_ref = args.reference == "on" or (args.reference == "auto" and N >= 2)
+    if want_ref:
+        if budget.fits(est["reference"]):
+            (ref_scores, _, _, full_s), _ = profiled_leg(
+                dataclasses.replace(r, mode=synth.CACHE_OFF), "full reference")
+            if N >= 2:
+                oc_h, of_h, rho, top1 = B.cs_rank(scores, ref_scores)
+                regret = float(ref_scores[of_h[0]] - ref_scores[oc_h[0]])
+        else:
+            skipped["reference"] = f"wall-clock budget (estimate {est['reference']:.0f} s, left {budget.left():.0f} s)"
+
     costs = None
     if full_s is not None:
-        cc = wall / args.steps / N
+        cc = rollout_s / N
         cf = full_s / N
         gamma = cc / cf
         costs = {"C_c_s": round(cc, 3), "C_f_s": round(cf, 3), "gamma": round(gamma, 4),
@@ -333,47 +470,80 @@ def main():
                  "keep_s": round(N * cc, 2), "commit_s": round(N * cc + cf, 2),
                  "best_of_N_full_s": round(N * cf, 2)}
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        progress("timing the CPU oracle on a sample")
-        try:
-            cpu = cpu_baseline(m, computed / (N * T * args.steps), nb)
-        except Exception as e:  # report, never hide
-            cpu = {"value": None, "error": repr(e)}
+    # ---- guided rollout (B = 2, w = 5): both branches evaluated per step
+    cfg_rec = None
+    if want_cfg_leg and mode != synth.CACHE_PAB:
+        if budget.fits(est["cfg"]):
+            cmasks = []
+            (sc2, c2, n2, s2), rates = profiled_leg(dataclasses.replace(r, n_branch=2), "guided (B=2)",
+                                                    record=cmasks)
+            cfg_rec = {"n_branch": 2, "guidance": r.guidance,
+                       "candidate_steps_per_s": round(N * T / s2, 4),
+                       "ms_per_step": round(s2 * 1e3 / T, 1),
+                       "skip_fraction": round(1 - c2 / n2, 4),
+                       "n_compute_histogram": n_compute_histogram(cmasks), "kernels": rates}
+        else:
+            skipped["cfg"] = f"wall-clock budget (estimate {est['cfg']:.0f} s, left {budget.left():.0f} s)"
+
+    # ---- tau sweep (ranked against the reference when it ran)
+    sweep = []
+    taus = ([0.05, 0.2] if mode == synth.CACHE_ADAPTIVE else []) if args.tau_sweep is None else \
+        [float(x) for x in args.tau_sweep.split(",") if x.strip()]
+    for tv in taus:
+        e = est["sweep_lower"] if tv < r.tau else est["sweep_higher"]
+        if not budget.fits(e):
+            skipped[f"tau={tv}"] = f"wall-clock budget (estimate {e:.0f} s, left {budget.left():.0f} s)"
+            continue
+        (sc, ct, nt, dt_s), _ = profiled_leg(dataclasses.replace(r, tau=tv), f"tau={tv}")
+        rec = {"tau": tv, "candidate_steps_per_s": round(N * T / dt_s, 4),
+               "skip_fraction": round(1 - ct / nt, 4), "ms_per_rollout": round(dt_s * 1e3, 1)}
+        if ref_scores is not None and N >= 2:
+            oc_t, of_t, rho_t, top1_t = B.cs_rank(sc, ref_scores)
+            rec.update({"rho_vs_full": rho_t, "top1_vs_full": top1_t,
+                        "regret": float(ref_scores[of_t[0]] - ref_scores[oc_t[0]])})
+        sweep.append(rec)
 
     out = {
         "metric": "cached candidate denoise-steps/s (N seeds, 1 GPU)",
         "value": round(value, 4),
         "unit": "candidate-steps/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": steps_timed,
+        "steps_requested": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 1),
+        "timed_rollouts": done,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32" if args.fp32 else "bf16",
         "data": "synthetic",
-        "config": {"workload": (f"{args.workload}: Wan-shaped DiT {m.n_blocks} blocks d={d} "
-                                f"{m.heads}x{m.head_dim} ffn={m.ffn}, {L} tokens, N={N} seeds, "
-                                f"T={T}, " + (f"PAB ranges self {r.pab_self} cross {r.pab_cross}"
-                                               if mode == synth.CACHE_PAB else
-                                               f"tau={r.tau}" if mode == synth.CACHE_ADAPTIVE else
-                                               f"static period {r.static_k}")
-                                + f", B={nb}, random init"),
+        "config": {"workload": args.workload,
+                   "description": (f"Wan-shaped DiT {m.n_blocks} blocks d={m.hidden} "
+                                   f"{m.heads}x{m.head_dim} ffn={m.ffn}, {m.tokens} tokens, N={N} seeds, "
+                                   f"T={T}, " + (f"PAB ranges self {r.pab_self} cross {r.pab_cross}"
+                                                  if mode == synth.CACHE_PAB else
+                                                  f"tau={r.tau}" if mode == synth.CACHE_ADAPTIVE else
+                                                  f"static period {r.static_k}")
+                                   + f", B={nb}, random init"),
                    "n_cand": N, "n_steps": T, "tau": r.tau, "n_branch": nb,
                    "cache_mode": r.mode},
         "skip_fraction": round(1.0 - computed / max(calls, 1), 4),
+        "n_compute_histogram": n_compute_histogram(masks),
         "attn_reuse_fraction": ({"self": round(reused[0] / max(calls, 1), 4),
                                  "cross": round(reused[1] / max(calls, 1), 4)}
                                 if mode == synth.CACHE_PAB else None),
         "rho_vs_full": rho,
         "top1_vs_full": top1,
-        "tau_sweep": sweep or None,
+        "regret_vs_full": regret,
         "costs": costs,
+        "cfg": cfg_rec,
+        "tau_sweep": sweep or None,
+        "skipped_legs": skipped or None,
         "roofline": roof,
         "cpu_baseline": cpu,
         "input_gen_s": round(gen_s, 1),
+        "bench_wall_s": round(budget.elapsed(), 1),
     }
     print(json.dumps(out), flush=True)
     gm.close()

@@ -114,6 +114,7 @@ typedef struct {
   int64_t computed;              /* calls evaluated by the transformer     */
   int64_t self_reused;           /* PAB: calls that reused the stored      */
   int64_t cross_reused;          /*   self / cross attention outputs       */
+  int32_t n_cand;                /* current candidate count (after retain) */
 } cs_rollout_stats_t;
 
 /* Kernel families timed by the optional profiler (cs_profile_*). */
@@ -172,7 +173,9 @@ void cs_rollout_free(cs_rollout* r);
  * the call is skipped iff a_ib <= tau (a call with ||xref|| = 0 computes).
  * override_mask: NULL, or host [n_cand][n_branch] bytes (1 = compute) that
  * replace the rule's decisions (replay); the indicator is still accumulated
- * and reported.  mask_out: NULL or host [n_cand][n_branch] (1 = compute).
+ * and reported.  An override that skips a call with no cached residual (in
+ * CS_CACHE_OFF mode, or before that branch's first computed call) is
+ * rejected with CS_E_INVAL before any device work.  mask_out: NULL or host [n_cand][n_branch] (1 = compute).
  * a_out: NULL or host [n_cand][n_branch], the indicator value compared with
  * tau at this step, NaN where the call was forced.  Calling it twice for
  * the same step returns CS_E_STATE.  In CS_CACHE_PAB mode every call
@@ -232,7 +235,13 @@ cs_status cs_rollout_import(cs_rollout* r, const void* buf, size_t bytes);
  * scores: lower index first) for both score vectors, and computes the
  * Spearman correlation of average ranks (NaN if a vector is constant) and
  * top-1 agreement (Sec. Experiments, definitions and protocol; Alg. 1's
- * argmax).  n >= 2 else CS_E_INVAL.  Any output pointer may be NULL. */
+ * argmax).  s_cached, s_full: host [n] doubles; order_cached, order_full:
+ * host [n] int32 (position 0 = best).  n >= 2 else CS_E_INVAL; scores must
+ * not be NaN.  Any output pointer may be NULL.
+ * Order only: with s_full == NULL only order_cached is written (n >= 1);
+ * order_full, rho and top1_agree must then be NULL (else CS_E_INVAL).  This
+ * is the ranking step of a search without a reference: keep mode's argmax
+ * (order_cached[0]) and the top-k of pruned search. */
 cs_status cs_rank(const double* s_cached, const double* s_full, int32_t n, int32_t* order_cached,
                   int32_t* order_full, double* rho, int32_t* top1_agree);
 

@@ -48,7 +48,7 @@ class cs_rollout_desc(C.Structure):
 
 class cs_rollout_stats_t(C.Structure):
     _fields_ = [("steps_done", C.c_int32), ("calls", C.c_int64), ("computed", C.c_int64),
-                ("self_reused", C.c_int64), ("cross_reused", C.c_int64)]
+                ("self_reused", C.c_int64), ("cross_reused", C.c_int64), ("n_cand", C.c_int32)]
 
 
 _lib: Optional[C.CDLL] = None
@@ -100,12 +100,34 @@ def _check(status: int) -> None:
         raise CsError(status, lib().cs_last_error().decode(errors="replace"))
 
 
-def _ptr(x) -> Optional[int]:
+def _ptr(x, numel: Optional[int] = None, dtype: str = "float32", name: str = "buffer") -> Optional[int]:
+    """Device address of ``x``: None, a raw integer address (passed through
+    unchecked), or a tensor, which must be a contiguous device tensor of the
+    given dtype holding at least ``numel`` elements."""
     if x is None:
         return None
     if isinstance(x, int):
         return x
+    if not getattr(x, "is_cuda", False):
+        raise ValueError(f"{name}: a device tensor is required (got {getattr(x, 'device', type(x))})")
+    if str(x.dtype).rsplit(".", 1)[-1] != dtype:
+        raise ValueError(f"{name}: dtype {x.dtype}, {dtype} required")
+    if not x.is_contiguous():
+        raise ValueError(f"{name}: tensor must be contiguous")
+    if numel is not None and x.numel() < numel:
+        raise ValueError(f"{name}: {x.numel()} elements, {numel} required")
     return int(x.data_ptr())
+
+
+# Latent size D of every live model handle and the model of every live
+# rollout handle, so that tensor arguments can be checked against the sizes
+# the library will read or write.
+_model_D = {}
+_rollout_model = {}
+
+
+def _latent_numel(model: int) -> Optional[int]:
+    return _model_D.get(model)
 
 
 def _stream(s) -> Optional[int]:
@@ -151,27 +173,42 @@ def cs_model_weight_count(desc: cs_model_desc) -> int:
 
 def cs_model_init(desc: cs_model_desc, weights, n_weights: int, stream=None) -> int:
     out = C.c_void_p()
-    _check(lib().cs_model_init(C.byref(desc), _ptr(weights), n_weights, _stream(stream), C.byref(out)))
+    _check(lib().cs_model_init(C.byref(desc), _ptr(weights, n_weights, name="weights"), n_weights,
+                               _stream(stream), C.byref(out)))
+    _model_D[out.value] = desc.in_ch * desc.lat_f * desc.lat_h * desc.lat_w
     return out.value
 
 
 def cs_model_free(model: int) -> None:
     lib().cs_model_free(model)
+    _model_D.pop(model, None)
 
 
 def cs_velocity(model: int, x, n: int, t: float, ctx, v) -> None:
-    _check(lib().cs_velocity(model, _ptr(x), n, float(t), _ptr(ctx), _ptr(v)))
+    D = _latent_numel(model)
+    nD = None if D is None else n * D
+    _check(lib().cs_velocity(model, _ptr(x, nD, name="x"), n, float(t), _ptr(ctx, name="ctx"),
+                             _ptr(v, nD, name="v")))
 
 
 def cs_rollout_init(model: int, desc: RolloutDesc, x1, ctx_cond, ctx_uncond=None) -> int:
     out = C.c_void_p()
-    _check(lib().cs_rollout_init(model, C.byref(desc.c), _ptr(x1), _ptr(ctx_cond), _ptr(ctx_uncond),
+    D = _latent_numel(model)
+    _check(lib().cs_rollout_init(model, C.byref(desc.c),
+                                 _ptr(x1, None if D is None else desc.c.n_cand * D, name="x1"),
+                                 _ptr(ctx_cond, name="ctx_cond"), _ptr(ctx_uncond, name="ctx_uncond"),
                                  C.byref(out)))
+    _rollout_model[out.value] = model
     return out.value
 
 
 def cs_rollout_free(r: int) -> None:
     lib().cs_rollout_free(r)
+    _rollout_model.pop(r, None)
+
+
+def _rollout_D(r: int) -> Optional[int]:
+    return _latent_numel(_rollout_model.get(r, 0))
 
 
 def cs_cache_decide(r: int, step: int, n_streams: int, override_mask: Optional[np.ndarray] = None,
@@ -193,14 +230,23 @@ def cs_denoise_step(r: int, step: int) -> None:
     _check(lib().cs_denoise_step(r, step))
 
 
+def _current_n_cand(r: int, n_cand: int) -> None:
+    cur = cs_rollout_stats(r).n_cand
+    if n_cand != cur:
+        raise ValueError(f"n_cand {n_cand} does not match the rollout's current {cur} candidates")
+
+
 def cs_score(r: int, w, n_cand: int) -> np.ndarray:
+    _current_n_cand(r, n_cand)
     out = np.zeros(n_cand, np.float64)
-    _check(lib().cs_score(r, _ptr(w), out.ctypes.data_as(C.POINTER(C.c_double))))
+    _check(lib().cs_score(r, _ptr(w, _rollout_D(r), name="w"), out.ctypes.data_as(C.POINTER(C.c_double))))
     return out
 
 
 def cs_rollout_latents(r: int, dst) -> None:
-    _check(lib().cs_rollout_latents(r, _ptr(dst)))
+    D = _rollout_D(r)
+    n = cs_rollout_stats(r).n_cand
+    _check(lib().cs_rollout_latents(r, _ptr(dst, None if D is None else n * D, name="dst")))
 
 
 def cs_rollout_enable_preview(r: int, on: bool = True) -> None:
@@ -208,8 +254,10 @@ def cs_rollout_enable_preview(r: int, on: bool = True) -> None:
 
 
 def cs_preview_score(r: int, w, n_cand: int) -> np.ndarray:
+    _current_n_cand(r, n_cand)
     out = np.zeros(n_cand, np.float64)
-    _check(lib().cs_preview_score(r, _ptr(w), out.ctypes.data_as(C.POINTER(C.c_double))))
+    _check(lib().cs_preview_score(r, _ptr(w, _rollout_D(r), name="w"),
+                                  out.ctypes.data_as(C.POINTER(C.c_double))))
     return out
 
 
@@ -237,18 +285,25 @@ def cs_rollout_import(r: int, data: bytes) -> None:
     _check(lib().cs_rollout_import(r, buf, len(data)))
 
 
-def cs_rank(s_cached: Sequence[float], s_full: Sequence[float]):
-    """(order_cached, order_full, rho, top1_agree)."""
+def cs_rank(s_cached: Sequence[float], s_full: Optional[Sequence[float]]):
+    """(order_cached, order_full, rho, top1_agree); with ``s_full`` None only
+    the order of ``s_cached`` is computed (the rest is None)."""
     a = np.ascontiguousarray(np.asarray(s_cached, np.float64))
-    b = np.ascontiguousarray(np.asarray(s_full, np.float64))
     n = a.size
     oc = np.zeros(n, np.int32)
+    pd = C.POINTER(C.c_double)
+    pi = C.POINTER(C.c_int32)
+    if s_full is None:
+        _check(lib().cs_rank(a.ctypes.data_as(pd), None, n, oc.ctypes.data_as(pi), None, None, None))
+        return oc.tolist(), None, None, None
+    b = np.ascontiguousarray(np.asarray(s_full, np.float64))
+    if b.size != n:
+        raise ValueError(f"score vectors of different lengths {n} and {b.size}")
     of = np.zeros(n, np.int32)
     rho = C.c_double(0.0)
     top1 = C.c_int32(0)
-    _check(lib().cs_rank(a.ctypes.data_as(C.POINTER(C.c_double)), b.ctypes.data_as(C.POINTER(C.c_double)),
-                         n, oc.ctypes.data_as(C.POINTER(C.c_int32)), of.ctypes.data_as(C.POINTER(C.c_int32)),
-                         C.byref(rho), C.byref(top1)))
+    _check(lib().cs_rank(a.ctypes.data_as(pd), b.ctypes.data_as(pd), n, oc.ctypes.data_as(pi),
+                         of.ctypes.data_as(pi), C.byref(rho), C.byref(top1)))
     return oc.tolist(), of.tolist(), rho.value, top1.value
 
 

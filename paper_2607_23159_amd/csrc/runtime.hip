@@ -795,6 +795,19 @@ static cs_status decide_impl(cs_rollout* r, int32_t step, const uint8_t* ovr, ui
   CHECK(r->decided_step != step, CS_E_STATE, "step %d already decided", step);
   CHECK(!(ovr && r->desc.mode == CS_CACHE_PAB), CS_E_UNSUPPORTED,
         "a replay override is not available in CS_CACHE_PAB mode");
+  if (ovr) {
+    // a skipped call applies the branch's cached residual: there must be one
+    // (CS_CACHE_OFF never stores it; before a branch's first computed call
+    // nothing is stored)
+    for (int s = 0; s < r->S; ++s) {
+      if (ovr[s]) continue;
+      CHECK(r->desc.mode != CS_CACHE_OFF, CS_E_INVAL,
+            "override skips stream %d, but CS_CACHE_OFF keeps no cached residual", s);
+      CHECK(r->has_ref_h[s], CS_E_INVAL,
+            "override skips stream %d at step %d before its first computed call (no cached residual)", s,
+            step);
+    }
+  }
   cs_model* m = r->model;
   hipStream_t st = m->stream;
   const cs_rollout_desc& d = r->desc;
@@ -990,6 +1003,7 @@ cs_status cs_rollout_stats(cs_rollout* r, cs_rollout_stats_t* out) {
     out->computed = r->computed;
     out->self_reused = r->self_reused;
     out->cross_reused = r->cross_reused;
+    out->n_cand = r->desc.n_cand;
     return CS_OK;
   })
 }
@@ -1055,10 +1069,16 @@ cs_status cs_rollout_import(cs_rollout* r, const void* buf, size_t bytes) {
 cs_status cs_rank(const double* sc, const double* sf, int32_t n, int32_t* order_c, int32_t* order_f,
                   double* rho, int32_t* top1) {
   GUARD({
-    CHECK(sc && sf, CS_E_INVAL, "score vectors must be non-NULL");
-    CHECK(n >= 2, CS_E_INVAL, "n must be >= 2");
+    CHECK(sc, CS_E_INVAL, "s_cached must be non-NULL");
+    if (!sf) {
+      CHECK(n >= 1, CS_E_INVAL, "n must be >= 1");
+      CHECK(!order_f && !rho && !top1, CS_E_INVAL,
+            "order_full, rho and top1_agree need s_full; pass NULL for them");
+    } else {
+      CHECK(n >= 2, CS_E_INVAL, "n must be >= 2");
+    }
     for (int i = 0; i < n; ++i)
-      CHECK(!(sc[i] != sc[i]) && !(sf[i] != sf[i]), CS_E_INVAL, "scores must not be NaN");
+      CHECK(!(sc[i] != sc[i]) && !(sf && sf[i] != sf[i]), CS_E_INVAL, "scores must not be NaN");
     auto order = [n](const double* s) {
       std::vector<int32_t> o(n);
       for (int i = 0; i < n; ++i) o[i] = i;
@@ -1080,8 +1100,10 @@ cs_status cs_rank(const double* sc, const double* sf, int32_t n, int32_t* order_
       }
       return r;
     };
-    const std::vector<int32_t> oc = order(sc), of = order(sf);
+    const std::vector<int32_t> oc = order(sc);
     if (order_c) memcpy(order_c, oc.data(), n * sizeof(int32_t));
+    if (!sf) return CS_OK;
+    const std::vector<int32_t> of = order(sf);
     if (order_f) memcpy(order_f, of.data(), n * sizeof(int32_t));
     if (top1) *top1 = oc[0] == of[0] ? 1 : 0;
     if (rho) {

@@ -148,8 +148,7 @@ def cached_search(model: GpuModel, wl: Workload, *, tau: Optional[float] = None,
     if full is not None:
         oc, of, rho, top1 = B.cs_rank(cached.scores, full.scores)
     else:
-        oc = sorted(range(len(cached.scores)), key=lambda i: (-cached.scores[i], i))
-        of, rho, top1 = None, None, None
+        oc, of, rho, top1 = B.cs_rank(cached.scores, None)
     win = oc[0]
     if mode == "commit":
         one = Workload(wl.name, wl.model, dataclasses.replace(wl.roll, n_cand=1), wl.weights, wl.ctx,
@@ -190,8 +189,8 @@ def pruned_search(model: GpuModel, wl: Workload, *, prune_step: int, keep: int,
         for k in range(1, prune_step + 1):
             B.cs_denoise_step(h, k)
         prev = B.cs_preview_score(h, inp.w, N)
-        order = sorted(range(N), key=lambda i: (-prev[i], i))
-        kept = sorted(order[:keep])
+        order, _, _, _ = B.cs_rank(prev, None)
+        kept = sorted(order[:keep])       # retain takes increasing indices
         B.cs_rollout_retain(h, kept)
         B.cs_rollout_enable_preview(h, False)
         for k in range(prune_step + 1, T + 1):
@@ -204,7 +203,7 @@ def pruned_search(model: GpuModel, wl: Workload, *, prune_step: int, keep: int,
         lat_np = lat.cpu().numpy().reshape((keep,) + wl.noise.shape[1:])
     finally:
         B.cs_rollout_free(h)
-    j = sorted(range(keep), key=lambda q: (-final[q], q))[0]
+    j = B.cs_rank(final, None)[0][0]
     win = kept[j]
     if mode == "commit":
         one = Workload(wl.name, wl.model, dataclasses.replace(r, n_cand=1), wl.weights, wl.ctx,

@@ -45,3 +45,62 @@ def compare_schedules(gpu_masks, ora_masks, ora_a, tau):
                 excused[s] = (k + 1, gap)
                 break
     return excused
+
+
+def token_errors(a, b, pt=1, ph=2, pw=2):
+    """Per-token error of latent ``a`` against ``b`` ([C][F][H][W]; a token
+    is one pt x ph x pw patch over all channels): ||a_t - b_t|| divided by
+    the RMS token norm of b.  The RMS of these values is the relative L2
+    error of the whole latent, so an error confined to a few tokens shows
+    here at full size instead of diluted by the token count."""
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    C, F, H, W = b.shape
+    def tok(x):
+        x = x.reshape(C, F // pt, pt, H // ph, ph, W // pw, pw)
+        return x.transpose(1, 3, 5, 0, 2, 4, 6).reshape((F // pt) * (H // ph) * (W // pw), -1)
+    ta, tb = tok(a), tok(b)
+    rms = math.sqrt(float(np.mean(np.sum(tb * tb, axis=1))))
+    return np.linalg.norm(ta - tb, axis=1) / max(rms, 1e-300)
+
+
+def row_errors(a, b):
+    """Per-row version of :func:`token_errors` for [rows][features] arrays
+    (sampled tokens of a patchified latent)."""
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    rms = math.sqrt(float(np.mean(np.sum(b * b, axis=1))))
+    return np.linalg.norm(a - b, axis=1) / max(rms, 1e-300)
+
+
+def order_desc(s):
+    """Candidates by decreasing score, equal scores lower index first."""
+    return sorted(range(len(s)), key=lambda i: (-float(s[i]), i))
+
+
+def discordant_pairs(order_ref, order_gpu):
+    """Pairs (x, y) that the reference ranks x above y and the GPU ranks y
+    above x."""
+    pos = {c: i for i, c in enumerate(order_gpu)}
+    out = []
+    for i in range(len(order_ref)):
+        for j in range(i + 1, len(order_ref)):
+            x, y = order_ref[i], order_ref[j]
+            if pos[x] > pos[y]:
+                out.append((x, y))
+    return out
+
+
+def check_ranking(s_gpu, s_ref, gap_tol, excused_cands=()):
+    """Rankings must match exactly.  A swapped pair is excused only if one
+    of its two candidates had an excused schedule flip, or the oracle's
+    score gap between the two is within ``gap_tol`` (4x the score error
+    measured on the replayed schedule).  Returns the discordant pairs."""
+    s_gpu = np.asarray(s_gpu, np.float64)
+    s_ref = np.asarray(s_ref, np.float64)
+    pairs = discordant_pairs(order_desc(s_ref), order_desc(s_gpu))
+    bad = [(x, y, float(abs(s_ref[x] - s_ref[y]))) for x, y in pairs
+           if x not in excused_cands and y not in excused_cands and abs(s_ref[x] - s_ref[y]) > gap_tol]
+    assert not bad, (f"unexcused ranking swaps (x, y, oracle gap) {bad}; gap tolerance {gap_tol:.3e}; "
+                     f"oracle order {order_desc(s_ref)}, gpu order {order_desc(s_gpu)}")
+    return pairs

@@ -113,3 +113,53 @@ def test_binding_fails_loudly_without_library(tmp_path):
             "b._lib = None\ntry:\n    b.lib()\nexcept RuntimeError as e:\n    print('raised', e)\n")
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT)
     assert "raised" in out.stdout and "not built" in out.stdout
+
+
+def test_cs_rank_order_only_form():
+    """With no full-rollout scores the library still orders the candidates
+    (keep mode's argmax, pruned search's top-k): decreasing score, ties to
+    the lower index, the same order the oracle's ranking gives; n = 1 is
+    allowed there; outputs that need the reference must be NULL."""
+    r = np.random.default_rng(11)
+    for _ in range(100):
+        n = int(r.integers(1, 12))
+        s = r.integers(0, 4, n).astype(float) if r.random() < 0.5 else r.standard_normal(n)
+        oc, of, rho, top1 = B.cs_rank(s, None)
+        assert of is None and rho is None and top1 is None
+        assert oc == orank.order_desc(list(s))
+    import ctypes as C
+    lib = B.lib()
+    a = (C.c_double * 3)(1.0, 2.0, 3.0)
+    o = (C.c_int32 * 3)()
+    rho = C.c_double()
+    assert lib.cs_rank(a, None, 3, o, None, C.byref(rho), None) == B.CS_E_INVAL
+    assert lib.cs_rank(a, None, 0, o, None, None, None) == B.CS_E_INVAL
+    assert lib.cs_rank(None, None, 3, o, None, None, None) == B.CS_E_INVAL
+
+
+def test_binding_checks_tensor_arguments():
+    """Tensors handed to the binding must be contiguous float32 device
+    tensors of at least the size the library will touch; the checks run
+    before any library call (here on the CPU, so every tensor is refused
+    for not being on a device)."""
+    import torch
+    with pytest.raises(ValueError, match="device tensor"):
+        B._ptr(torch.zeros(4), name="x")
+    class Fake:
+        is_cuda = True
+        def __init__(self, dtype, contig=True, n=8):
+            self.dtype, self._c, self._n = dtype, contig, n
+        def is_contiguous(self):
+            return self._c
+        def numel(self):
+            return self._n
+        def data_ptr(self):
+            return 4096
+    assert B._ptr(Fake(torch.float32), 8) == 4096
+    with pytest.raises(ValueError, match="dtype"):
+        B._ptr(Fake(torch.float16), 8)
+    with pytest.raises(ValueError, match="contiguous"):
+        B._ptr(Fake(torch.float32, contig=False), 8)
+    with pytest.raises(ValueError, match="elements"):
+        B._ptr(Fake(torch.float32, n=7), 8)
+    assert B._ptr(None) is None and B._ptr(1234) == 1234

@@ -61,3 +61,66 @@ def test_committed_traffic_summary_is_well_formed():
     v = bench.measured_traffic("wan13b_cached", 1)
     current = fields["- kernel_source_sha256"].strip().strip("`") == bench.attn_source_hash()
     assert (v is not None) == current
+
+
+# ---------------------------------------------------------------- step units
+def test_timed_rollouts_round_up_to_whole_rollouts():
+    assert bench.timed_rollouts(20, 50) == 1      # the driver's --steps 20 at T = 50
+    assert bench.timed_rollouts(50, 50) == 1
+    assert bench.timed_rollouts(51, 50) == 2
+    assert bench.timed_rollouts(100, 50) == 2
+    assert bench.timed_rollouts(1, 10) == 1
+    assert bench.timed_rollouts(25, 10) == 3
+    with pytest.raises(ValueError):
+        bench.timed_rollouts(0, 50)
+
+
+def test_default_arguments_time_one_rollout_with_warmup_steps():
+    a = bench.parse([])
+    assert (a.steps, a.warmup, a.gpus, a.workload) == (50, 5, 1, "wan13b_cached")
+    assert bench.timed_rollouts(a.steps, 50) == 1
+    d = bench.parse(["--steps", "20", "--warmup", "5"])
+    assert bench.timed_rollouts(d.steps, 50) == 1
+    with pytest.raises(SystemExit):
+        bench.parse(["--steps", "0"])
+    with pytest.raises(SystemExit):
+        bench.parse(["--warmup", "-1"])
+
+
+def test_budget_refuses_a_leg_that_would_overrun():
+    now = [100.0]
+    b = bench.Budget(480.0, start=100.0, clock=lambda: now[0])
+    assert b.fits(480.0) and not b.fits(480.5)
+    now[0] = 400.0                        # 300 s used
+    assert b.elapsed() == 300.0 and b.left() == 180.0
+    assert b.fits(179.0) and not b.fits(181.0)
+
+
+def test_leg_estimates_scale_with_the_measured_rollout():
+    # 40 s rollout of N = 8, T = 50, B = 1 with 160 of 400 calls computed
+    e = bench.leg_estimates(40.0, 160, 8, 50, 1)
+    assert e["reference"] == pytest.approx(40.0 / 160 * 400 * 1.05)     # 105 s
+    assert e["cfg"] == pytest.approx(40.0 * 2.0 * 1.15)
+    assert e["sweep_higher"] == pytest.approx(42.0)
+    assert e["sweep_lower"] == pytest.approx(54.0)
+    # nothing computed beyond the forced steps cannot make the full rollout cheaper than it is
+    e0 = bench.leg_estimates(10.0, 0, 4, 10, 2)
+    assert e0["reference"] > 0
+    # a worst-case driver run fits the default budget: 2 min of start-up,
+    # 20 s of inputs, 5 warmup steps, the timed rollout, the CPU leg and
+    # every optional leg at the measured 1.3B rates
+    total = 120 + 20 + 4 + 40 + 15 + e["reference"] + e["cfg"] + e["sweep_lower"] + e["sweep_higher"]
+    assert total < 600
+
+
+def test_n_compute_histogram_counts_steps_per_batch_size():
+    import numpy as np
+    masks = [np.array([1, 1, 1, 1], np.uint8)] * 5 + [np.array([1, 0, 1, 0], np.uint8)] * 2 + \
+        [np.zeros(4, np.uint8)] * 3
+    assert bench.n_compute_histogram(masks) == {"0": 3, "2": 2, "4": 5}
+    assert bench.n_compute_histogram([]) == {}
+
+
+def test_cpu_model_name_is_a_string():
+    s = bench.cpu_model_name()
+    assert isinstance(s, str) and s

@@ -119,6 +119,22 @@ def test_rope_matches_complex_formulation_and_identities():
     assert ang[tok(1, 0, 0), 1] == pytest.approx(10000.0 ** (-1.0 / n_f))
 
 
+def test_rope_angles_match_hand_derived_table():
+    """Every band's frequencies, not only pair 0: hand-derived angles
+    (powers of ten) at tokens away from the origin on all three axes, for
+    head dims 32 and 128 (a wrong band split, denominator or axis order
+    moves at least one entry)."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "rope_angles.json")))
+    for e in g["entries"]:
+        grid = tuple(e["grid"])
+        ang = dit.rope_angles(grid, e["head_dim"])
+        f, h, w = e["token"]
+        tok = (f * grid[1] + h) * grid[2] + w
+        assert ang[tok, e["pair"]] == pytest.approx(e["value"], rel=1e-11, abs=1e-15), e
+
+
 def test_time_sinusoid_values():
     s = dit.time_sinusoid(0.0, 256)
     np.testing.assert_array_equal(s[:128], np.ones(128))
@@ -152,7 +168,17 @@ def _torch_velocity(x, t, ctx, W, m):
                  T["text2_w"], T["text2_b"])
     tok = einops.rearrange(t64(x), "c (f pt) (h ph) (w pw) -> (f h w) (c pt ph pw)", pt=1, ph=2, pw=2)
     z = F.linear(tok, T["patch_w"], T["patch_b"])
-    ang = t64(dit.rope_angles(m.grid, dh))
+    # rotary angles built here from positions and per-band frequencies (not
+    # from the oracle's table)
+    nf_b = dh // 2 - 2 * (dh // 6)
+    nhw_b = dh // 6
+    freq = lambda n: torch.pow(torch.tensor(10000.0, dtype=torch.float64),
+                               -torch.arange(n, dtype=torch.float64) / n)
+    gf, gh, gw = m.grid
+    pf, ph_, pw_ = torch.meshgrid(torch.arange(gf, dtype=torch.float64), torch.arange(gh, dtype=torch.float64),
+                                  torch.arange(gw, dtype=torch.float64), indexing="ij")
+    ang = torch.cat([pf.reshape(-1, 1) * freq(nf_b), ph_.reshape(-1, 1) * freq(nhw_b),
+                     pw_.reshape(-1, 1) * freq(nhw_b)], dim=1)
     rot = torch.polar(torch.ones_like(ang), ang)[:, None, :]
     L = z.shape[0]
 
