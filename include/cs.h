@@ -198,6 +198,25 @@ cs_status cs_denoise_step(cs_rollout* r, int32_t step);
  * scores: host [n_cand] double.  Synchronises. */
 cs_status cs_score(cs_rollout* r, const float* w, double* scores);
 
+/* Allocation-free scoring, for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops or harnesses that forbid
+ * hipMalloc): the scores of cs_score, s_i = <w, x_i> / sqrt(D) summed in
+ * fp64 in the same fixed order (bitwise equal to cs_score on the same
+ * latents), for n latents the caller holds, without a rollout handle.
+ * x: device [n][D] float32, w: device [D] float32, both 16-byte aligned;
+ * D % 4 == 0; scores: device [n] double (written); stream: hipStream_t or
+ * NULL.  Only enqueues work (no synchronisation, no allocation, no memset).
+ * The per-chunk partial sums go to a static device array owned by the
+ * library, CS_SCORE_NOALLOC_MAX_PARTIALS doubles (4 MiB) per GPU, held until
+ * the process ends; n * ceil(D / 8192) above that capacity returns
+ * CS_E_INVAL before any device work.  Every call on one GPU shares that
+ * array and it keeps the last call's contents: calls that overlap on one
+ * GPU (different streams, or host threads) race and must be serialised by
+ * the caller. */
+#define CS_SCORE_NOALLOC_MAX_PARTIALS (512 * 1024)
+cs_status cs_score_noalloc(const float* x, const float* w, int32_t n, int64_t D, double* scores,
+                           void* stream);
+
 /* Pruned composition (Sec. Composition with pruned search).
  * cs_rollout_enable_preview(r, 1) makes every following cs_denoise_step also
  * keep the guided velocity v~ of that step (one extra [n_cand][D] fp32

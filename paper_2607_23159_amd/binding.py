@@ -73,6 +73,7 @@ def lib() -> C.CDLL:
         "cs_cache_decide": (i32, [vp, i32, pu8, pu8, pd]),
         "cs_denoise_step": (i32, [vp, i32]),
         "cs_score": (i32, [vp, pf, pd]),
+        "cs_score_noalloc": (i32, [pf, pf, i32, i64, pf, vp]),
         "cs_rollout_latents": (i32, [vp, pf]),
         "cs_rollout_stats": (i32, [vp, C.POINTER(cs_rollout_stats_t)]),
         "cs_rollout_enable_preview": (i32, [vp, i32]),
@@ -241,6 +242,13 @@ def cs_score(r: int, w, n_cand: int) -> np.ndarray:
     out = np.zeros(n_cand, np.float64)
     _check(lib().cs_score(r, _ptr(w, _rollout_D(r), name="w"), out.ctypes.data_as(C.POINTER(C.c_double))))
     return out
+
+
+def cs_score_noalloc(x, w, n: int, D: int, scores, stream=None) -> None:
+    """Enqueue the scores of n latents x [n][D] into the device float64
+    tensor ``scores`` [n]; allocates nothing and does not synchronise."""
+    _check(lib().cs_score_noalloc(_ptr(x, n * D, name="x"), _ptr(w, D, name="w"), int(n), int(D),
+                                  _ptr(scores, n, dtype="float64", name="scores"), _stream(stream)))
 
 
 def cs_rollout_latents(r: int, dst) -> None:

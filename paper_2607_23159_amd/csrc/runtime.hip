@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -519,6 +520,34 @@ static cs_status ctx_dispatch(cs_model* m, CtxKV& c, int b, const float* ctx) {
   return build_ctx<float>(m, c, b, ctx);
 }
 
+// ------------------------------------------------- allocation-free scoring
+// Partial sums of cs_score_noalloc live in this file-scope device array (one
+// copy per GPU, held until the process ends).  In host code `scratch` only
+// names the symbol: its device address is looked up once per device with
+// hipGetSymbolAddress and every launch takes that address.
+static __device__ __align__(256) double scratch[CS_SCORE_NOALLOC_MAX_PARTIALS];
+
+static constexpr int MAX_DEVICES = 64;
+static double* g_scratch_ptr[MAX_DEVICES] = {nullptr};
+static std::mutex g_scratch_mu;
+
+// Device address of `scratch` on the current device (looked up on the
+// first call made with that device current).
+static cs_status scratch_ptr(double** out) {
+  int dev = -1;
+  HIPC(hipGetDevice(&dev));
+  CHECK(dev >= 0 && dev < MAX_DEVICES, CS_E_UNSUPPORTED, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIPC(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    CHECK(p, CS_E_DEVICE, "hipGetSymbolAddress returned NULL for the scoring scratch array");
+    g_scratch_ptr[dev] = static_cast<double*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return CS_OK;
+}
+
 // ================================================================ C ABI
 extern "C" {
 
@@ -905,6 +934,30 @@ cs_status cs_score(cs_rollout* r, const float* w, double* scores) {
     HIPC(hipMemcpyAsync(r->scores_host, r->scores, r->desc.n_cand * sizeof(double), hipMemcpyDeviceToHost, st));
     HIPC(hipStreamSynchronize(st));
     memcpy(scores, r->scores_host, r->desc.n_cand * sizeof(double));
+    return CS_OK;
+  })
+}
+
+cs_status cs_score_noalloc(const float* x, const float* w, int32_t n, int64_t D, double* scores,
+                           void* stream) {
+  GUARD({
+    CHECK(x && w && scores, CS_E_INVAL, "x, w and scores must be non-NULL");
+    CHECK(n >= 1 && n <= 65535, CS_E_INVAL, "n must be in [1, 65535]");
+    CHECK(D >= 4 && D % 4 == 0, CS_E_INVAL, "D must be a positive multiple of 4");
+    CHECK(((uintptr_t)x % 16) == 0 && ((uintptr_t)w % 16) == 0, CS_E_INVAL,
+          "x and w must be 16-byte aligned");
+    CHECK(((uintptr_t)scores % 8) == 0, CS_E_INVAL, "scores must be 8-byte aligned");
+    const long nchunk = score_chunks((long)D);
+    CHECK((long)n * nchunk <= (long)CS_SCORE_NOALLOC_MAX_PARTIALS, CS_E_INVAL,
+          "n * ceil(D / 8192) = %ld partial sums exceed the scratch capacity of %ld", (long)n * nchunk,
+          (long)CS_SCORE_NOALLOC_MAX_PARTIALS);
+    double* part = nullptr;
+    TRY(scratch_ptr(&part));
+    hipStream_t st = (hipStream_t)stream;
+    // every partial the finalize reads is written by the partials kernel of
+    // this call first (same stream), so the array needs no clearing
+    HIPC(score_partials(x, nullptr, 0.0f, w, n, (long)D, part, st));
+    HIPC(score_finalize(part, n, (int)nchunk, (long)D, scores, st));
     return CS_OK;
   })
 }
