@@ -21,7 +21,10 @@ does not fit is reported as skipped, never started):
     analysis: C_c, C_f, gamma, break-even N);
   * one guided rollout (B = 2, w = 5, both branches evaluated per step);
   * the tau sweep, one cached rollout per extra tau, ranked against the
-    same reference.
+    same reference;
+  * the static schedule (every k-th step between the forced windows) with
+    the period whose skip fraction is closest to the headline's, ranked
+    against the same reference.
 
 Printed: one JSON line with the metric, the roofline of the dominant kernel
 (self-attention, timed by HIP events on the rollout stream inside the
@@ -120,7 +123,31 @@ def leg_estimates(rollout_s: float, computed: int, n_cand: int, n_steps: int, n_
         # a smaller tau computes more: bounded by the full rollout
         "sweep_lower": min(full, rollout_s * 1.35),
         "sweep_higher": rollout_s * 1.05,
+        # the static schedule at the same skip fraction computes about as much
+        "static": rollout_s * 1.1,
     }
+
+
+def static_computes(n_steps: int, k_warm: int, k_cool: int, period: int) -> int:
+    """Computed steps per stream of the static schedule (the uniform baseline
+    of Sec. Method, properties): the forced windows, the first step (no
+    cached residual yet), and every period-th step between the windows."""
+    n = 0
+    for s in range(1, n_steps + 1):
+        window = s <= k_warm or s > n_steps - k_cool
+        n += window or s == 1 or (s - k_warm) % period == 0
+    return n
+
+
+def matched_static_period(n_steps: int, k_warm: int, k_cool: int, skip_fraction: float) -> int:
+    """Static period whose skip fraction is closest to ``skip_fraction``
+    (ties: the shorter period, which computes more)."""
+    best, best_gap = 1, float("inf")
+    for k in range(1, n_steps + 1):
+        gap = abs(1.0 - static_computes(n_steps, k_warm, k_cool, k) / n_steps - skip_fraction)
+        if gap < best_gap - 1e-12:
+            best, best_gap = k, gap
+    return best
 
 
 def n_compute_histogram(masks) -> dict:
@@ -165,6 +192,14 @@ def parse(argv=None):
                    help="reuse engine: the drift-indicator cache, the static schedule, or "
                         "attention-output broadcasting")
     p.add_argument("--static-k", type=int, default=None, help="static schedule period")
+    p.add_argument("--no-static-leg", action="store_true",
+                   help="skip the static-schedule rollout at the headline's skip fraction")
+    p.add_argument("--init", choices=["paper", "stress"], default="paper",
+                   help="weight init: the workload's N(0, 0.02), or the test-only stress init")
+    p.add_argument("--k-warm", type=int, default=None, help="forced warmup steps")
+    p.add_argument("--k-cool", type=int, default=None, help="forced cooldown steps")
+    p.add_argument("--decision-log", default=None,
+                   help="write the timed rollout's per-call cache decisions as JSON lines")
     p.add_argument("--pab-self", type=int, default=2, help="self-attention broadcast range")
     p.add_argument("--pab-cross", type=int, default=6, help="cross-attention broadcast range")
     p.add_argument("--calibration-copy", type=int, default=0,
@@ -277,10 +312,14 @@ def main(argv=None):
     mode = {"adaptive": synth.CACHE_ADAPTIVE, "static": synth.CACHE_STATIC,
             "pab": synth.CACHE_PAB}[args.mode]
     extra = {} if args.static_k is None else {"static_k": args.static_k}
+    if args.k_warm is not None:
+        extra["k_warm"] = args.k_warm
+    if args.k_cool is not None:
+        extra["k_cool"] = args.k_cool
     # the guided leg needs the unconditional context: draw it whenever that
     # leg may run (the headline's own inputs do not change)
     want_cfg_leg = nb == 1 and not args.no_cfg_leg
-    wl = synth.make_workload(args.workload, n_branch=2 if want_cfg_leg else nb, dtype=dtype,
+    wl = synth.make_workload(args.workload, n_branch=2 if want_cfg_leg else nb, dtype=dtype, init=args.init,
                              n_cand=args.n_cand, n_steps=args.n_steps, tau=args.tau, mode=mode,
                              pab_self=args.pab_self, pab_cross=args.pab_cross, **extra)
     m = wl.model
@@ -295,7 +334,7 @@ def main(argv=None):
     S = N * nb
     R = timed_rollouts(args.steps, T)
 
-    def rollout(roll, label, record=None, counters=None):
+    def rollout(roll, label, record=None, counters=None, a_record=None):
         """One rollout of ``roll``; returns (scores, computed, calls, seconds)."""
         desc = B.RolloutDesc(roll, wl.timesteps)
         torch.cuda.synchronize()
@@ -304,8 +343,10 @@ def main(argv=None):
         try:
             for k in range(1, roll.n_steps + 1):
                 if record is not None:
-                    mk, _ = B.cs_cache_decide(h, k, roll.n_cand * roll.n_branch)
+                    mk, av = B.cs_cache_decide(h, k, roll.n_cand * roll.n_branch)
                     record.append(mk.copy())
+                    if a_record is not None:
+                        a_record.append(av.copy())
                 B.cs_denoise_step(h, k)
                 if k % 10 == 0:
                     progress(f"{label} rollout: step {k}/{roll.n_steps}")
@@ -352,12 +393,13 @@ def main(argv=None):
     computed = calls = 0
     reused = [0, 0]
     masks = []
+    avals = []
     scores = None
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     done = 0
     for i in range(R):
-        scores, c, n, _ = rollout(r, f"timed {i + 1}/{R}", record=masks, counters=reused)
+        scores, c, n, _ = rollout(r, f"timed {i + 1}/{R}", record=masks, counters=reused, a_record=avals)
         computed += c
         calls += n
         done += 1
@@ -372,6 +414,10 @@ def main(argv=None):
     value = N * steps_timed / wall
     rollout_s = wall / done
     progress(f"headline: {value:.3f} candidate-steps/s ({rollout_s:.1f} s per rollout)")
+    if args.decision_log:
+        from paper_2607_23159_amd.search import write_decision_log
+        nrec = write_decision_log(args.decision_log, np.array(masks[:T]), np.array(avals[:T]), nb)
+        progress(f"{nrec} decision records written to {args.decision_log}")
 
     roof = None
     fam = {}
@@ -503,6 +549,25 @@ def main(argv=None):
                         "regret": float(ref_scores[of_t[0]] - ref_scores[oc_t[0]])})
         sweep.append(rec)
 
+    # ---- static schedule at the adaptive rule's skip fraction (Sec. Method,
+    # properties: the uniform baseline), ranked against the same reference
+    static_rec = None
+    if mode == synth.CACHE_ADAPTIVE and not args.no_static_leg:
+        skip_a = 1.0 - computed / max(calls, 1)
+        k_s = matched_static_period(T, r.k_warm, r.k_cool, skip_a)
+        if budget.fits(est["static"]):
+            (sc_s, c_s, n_s, s_s), _ = profiled_leg(
+                dataclasses.replace(r, mode=synth.CACHE_STATIC, static_k=k_s), f"static k={k_s}")
+            static_rec = {"static_k": k_s, "skip_fraction": round(1 - c_s / n_s, 4),
+                          "adaptive_skip_fraction": round(skip_a, 4),
+                          "candidate_steps_per_s": round(N * T / s_s, 4)}
+            if ref_scores is not None and N >= 2:
+                oc_s, of_s, rho_s, top1_s = B.cs_rank(sc_s, ref_scores)
+                static_rec.update({"rho_vs_full": rho_s, "top1_vs_full": top1_s,
+                                   "regret": float(ref_scores[of_s[0]] - ref_scores[oc_s[0]])})
+        else:
+            skipped["static"] = f"wall-clock budget (estimate {est['static']:.0f} s, left {budget.left():.0f} s)"
+
     out = {
         "metric": "cached candidate denoise-steps/s (N seeds, 1 GPU)",
         "value": round(value, 4),
@@ -525,7 +590,8 @@ def main(argv=None):
                                                   if mode == synth.CACHE_PAB else
                                                   f"tau={r.tau}" if mode == synth.CACHE_ADAPTIVE else
                                                   f"static period {r.static_k}")
-                                   + f", B={nb}, random init"),
+                                   + f", B={nb}, " + ("random init" if args.init == "paper"
+                                                      else "stress init (test-only)")),
                    "n_cand": N, "n_steps": T, "tau": r.tau, "n_branch": nb,
                    "cache_mode": r.mode},
         "skip_fraction": round(1.0 - computed / max(calls, 1), 4),
@@ -539,6 +605,7 @@ def main(argv=None):
         "costs": costs,
         "cfg": cfg_rec,
         "tau_sweep": sweep or None,
+        "static_schedule": static_rec,
         "skipped_legs": skipped or None,
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -70,6 +70,33 @@ class GpuRollout:
         return [bool(m) for m in self.masks[:, i * n_branch + b]]
 
 
+def decision_records(masks: np.ndarray, a: np.ndarray, n_branch: int, computed_by: str = "rule"):
+    """Per-call decision records of a rollout from its [T][S] masks and
+    indicator values (S = N * n_branch, stream s = candidate s // n_branch,
+    branch s % n_branch): step k (1-based), candidate i, branch b, the
+    indicator a compared with tau at that call (None where the call was
+    forced), and the decision ("compute" or "skip")."""
+    T, S = masks.shape
+    out = []
+    for k in range(T):
+        for st in range(S):
+            av = float(a[k, st])
+            out.append({"k": k + 1, "i": st // n_branch, "b": st % n_branch,
+                        "a": None if np.isnan(av) else av,
+                        "decision": "compute" if masks[k, st] else "skip"})
+    return out
+
+
+def write_decision_log(path: str, masks: np.ndarray, a: np.ndarray, n_branch: int) -> int:
+    """Write the decision records as JSON lines; returns the record count."""
+    import json
+    recs = decision_records(masks, a, n_branch)
+    with open(path, "w") as f:
+        for r in recs:
+            f.write(json.dumps(r) + "\n")
+    return len(recs)
+
+
 class Inputs:
     """Device copies of a workload's per-rollout inputs."""
 

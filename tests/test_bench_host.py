@@ -124,3 +124,48 @@ def test_n_compute_histogram_counts_steps_per_batch_size():
 def test_cpu_model_name_is_a_string():
     s = bench.cpu_model_name()
     assert isinstance(s, str) and s
+
+
+@pytest.mark.parametrize("T,kw,kc", [(50, 5, 5), (10, 1, 1), (12, 0, 0), (8, 2, 3), (1, 0, 0)])
+def test_static_computes_matches_the_oracle_schedule(T, kw, kc):
+    """The bench's count of computed steps per stream under the static
+    schedule equals what the oracle's rollout computes (velocity -x, any
+    latent), for every period."""
+    import numpy as np
+    from oracle import rollout as orl
+    x1 = np.ones((1, 2, 1, 2, 2))
+    fns = [lambda x, t: -x]
+    grid = [1.0 - k / T for k in range(T + 1)]
+    for k in range(1, T + 2):
+        res = orl.cached_rollout(x1, fns, grid, tau=0.0, k_warm=kw, k_cool=kc, guidance=1.0,
+                                 mode=orl.CACHE_STATIC, static_k=k)
+        assert bench.static_computes(T, kw, kc, k) == res.n_compute, (T, kw, kc, k)
+
+
+def test_matched_static_period():
+    # T = 50, windows 5/5: period 4 computes 10 + 10 = 20 of 50 (skip 0.6)
+    assert bench.static_computes(50, 5, 5, 4) == 20
+    assert bench.matched_static_period(50, 5, 5, 0.6) == 4
+    assert bench.matched_static_period(50, 5, 5, 0.0) == 1
+    # the closest achievable fraction, shorter period on ties
+    k = bench.matched_static_period(50, 5, 5, 0.56)
+    fr = lambda k: 1 - bench.static_computes(50, 5, 5, k) / 50
+    assert all(abs(fr(k) - 0.56) <= abs(fr(j) - 0.56) for j in range(1, 51))
+
+
+def test_decision_log_records(tmp_path):
+    """The decision log has one JSON line per (step, candidate, branch) with
+    the indicator (null where the call was forced) and the decision."""
+    import json
+    import numpy as np
+    from paper_2607_23159_amd.search import decision_records, write_decision_log
+    masks = np.array([[1, 1, 1, 1], [0, 1, 0, 0], [1, 1, 1, 1]], np.uint8)
+    a = np.array([[np.nan] * 4, [0.05, 0.2, 0.07, 0.09], [np.nan] * 4])
+    p = tmp_path / "d.jsonl"
+    assert write_decision_log(str(p), masks, a, 2) == 12
+    recs = [json.loads(l) for l in p.read_text().splitlines()]
+    assert recs == decision_records(masks, a, 2)
+    assert recs[0] == {"k": 1, "i": 0, "b": 0, "a": None, "decision": "compute"}
+    assert recs[5] == {"k": 2, "i": 0, "b": 1, "a": 0.2, "decision": "compute"}
+    assert recs[6] == {"k": 2, "i": 1, "b": 0, "a": 0.07, "decision": "skip"}
+    assert sum(r["decision"] == "skip" for r in recs) == 3

@@ -370,3 +370,61 @@ def test_checkpoint_resume_bitwise():
     torch.cuda.synchronize()
     B.cs_rollout_free(h2)
     assert np.array_equal(out.cpu().numpy().reshape(ref.latents.shape), ref.latents)
+
+
+@pytest.mark.parametrize("dtype", [synth.DTYPE_FP32, synth.DTYPE_BF16])
+def test_static_schedule_at_the_adaptive_skip_fraction(dtype):
+    """The uniform baseline at a matched budget: the static period whose
+    skip fraction is closest to the adaptive rule's (tau = 0.1) is run on the
+    GPU and in the oracle; schedules equal, latents within the bar, and both
+    rankings are compared with the full rollouts' on each side (the GPU's
+    rho / top-1 must equal the oracle's unless a near tie)."""
+    import bench
+    gm, m = gpu_model("tiny", dtype, "stress")
+    wl = workload("tiny", 1, "stress", dtype)
+    r = wl.roll
+    res_a = oracle_rollout(wl, 0.1, key=("tiny", 1))
+    skip = 1.0 - res_a.n_compute / res_a.n_calls
+    k = bench.matched_static_period(r.n_steps, r.k_warm, r.k_cool, skip)
+    say(f"static at matched skip: adaptive skip {skip:.2f}, period {k}")
+    import dataclasses
+    wl_s = synth.Workload(wl.name, wl.model, dataclasses.replace(r, mode=synth.CACHE_STATIC, static_k=k),
+                          wl.weights, wl.ctx, wl.noise, wl.scorer, wl.timesteps)
+    g = run_rollout(gm, wl_s)
+    res_s = orl.run_workload(wl_s)
+    om, _ = oracle_masks(res_s, r.n_cand, 1, r.n_steps)
+    assert np.array_equal(g.masks, om)
+    assert g.computed == res_s.n_compute == r.n_cand * bench.static_computes(r.n_steps, r.k_warm, r.k_cool, k)
+    for i in range(r.n_cand):
+        assert rel_l2(g.latents[i], res_s.latents[i]) < TOL[dtype]
+    s_ref = orl.score(res_s.latents, wl.scorer)
+    check_ranking(g.scores, s_ref, 4 * np.abs(g.scores - s_ref).max())
+    full = oracle_rollout(wl, 0.0, mode=orl.CACHE_OFF, key=("tiny", 1))
+    f_ref = orl.score(full.latents, wl.scorer)
+    _, _, rho_o, top1_o, _ = orank.rank_report(list(s_ref), list(f_ref))
+    g_full = run_rollout(gm, wl, mode=synth.CACHE_OFF)
+    _, _, rho_g, top1_g = B.cs_rank(g.scores, g_full.scores)
+    say(f"  static: rho gpu {rho_g} oracle {rho_o}, top-1 gpu {top1_g} oracle {top1_o}")
+    if np.min(np.diff(np.sort(s_ref))) > 4 * np.abs(g.scores - s_ref).max() and \
+            np.min(np.diff(np.sort(f_ref))) > 4 * np.abs(g_full.scores - f_ref).max():
+        assert rho_g == pytest.approx(rho_o, abs=1e-12) and top1_g == top1_o
+
+
+def test_decision_log_matches_oracle_log():
+    """The per-call decision log written from a GPU rollout (fp32 path,
+    tau = 0.1) equals the oracle's own decision log call by call: same
+    decisions, forced calls without an indicator, indicators within 1e-6."""
+    from paper_2607_23159_amd.search import decision_records
+    gm, m = gpu_model("tiny", synth.DTYPE_FP32, "stress")
+    wl = workload("tiny", 2, "stress", synth.DTYPE_FP32)
+    res = oracle_rollout(wl, 0.1, key=("tiny", 2))
+    g = run_rollout(gm, wl, tau=0.1)
+    recs = {(d["k"], d["i"], d["b"]): d for d in decision_records(g.masks, g.a, 2)}
+    assert len(recs) == len(res.log) == wl.roll.n_cand * 2 * wl.roll.n_steps
+    for o in res.log:
+        d = recs[(o.k, o.i, o.b)]
+        assert d["decision"] == ("compute" if o.compute else "skip"), (o, d)
+        if o.a is None:
+            assert d["a"] is None
+        else:
+            assert d["a"] == pytest.approx(o.a, rel=1e-6)
