@@ -211,12 +211,23 @@ def parse(argv=None):
     return a
 
 
-def cpu_baseline(model_cfg, computed_per_cand_step: float, n_branch: int):
-    """The float64 oracle on a bounded sample of the workload: one
-    transformer block at full token count with R1 and R2 sampled query rows
-    (keys/values of all tokens), extrapolated linearly to all rows, times
-    the block count, times the transformer calls per candidate-step the GPU
-    run measured."""
+ORACLE_FULL_ROLLOUT_FLOP = 1.0e12   # below this the oracle runs the whole rollout (~20 s in fp64)
+
+
+def eval_flop(m) -> float:
+    """Algorithmic FLOP of one transformer call: projections and FFN, and
+    the self-attention products (text keys/values are per rollout)."""
+    L, d = m.tokens, m.hidden
+    return 2.0 * L * m.n_blocks * (6 * d * d + 2 * d * m.ffn) + 4.0 * L * L * d * m.n_blocks
+
+
+def cpu_baseline(model_cfg, computed_per_cand_step: float, n_branch: int, wl=None):
+    """The float64 oracle timed on the host.  Small workloads (the tiny
+    configuration): the whole cached rollout of the workload, timed
+    directly.  Large ones: a bounded sample, one transformer block at full
+    token count with R1 and R2 sampled query rows (keys/values of all
+    tokens), extrapolated linearly to all rows, times the block count, times
+    the transformer calls per candidate-step the GPU run measured."""
     import dataclasses
 
     import numpy as np
@@ -229,6 +240,18 @@ def cpu_baseline(model_cfg, computed_per_cand_step: float, n_branch: int):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count() or 1
+    if wl is not None:
+        r = wl.roll
+        if eval_flop(model_cfg) * r.n_cand * r.n_branch * r.n_steps <= ORACLE_FULL_ROLLOUT_FLOP:
+            from oracle import rollout as orl
+            t0 = time.perf_counter()
+            res = orl.run_workload(wl)
+            el = time.perf_counter() - t0
+            return {"value": r.n_cand * r.n_steps / el, "unit": "candidate-steps/s", "cores": int(cores),
+                    "cpu_model": cpu_model_name(), "kind": "oracle",
+                    "sample": (f"float64 oracle, the whole cached rollout of the workload ({r.n_cand} seeds x "
+                               f"{r.n_steps} steps, B={r.n_branch}, tau={r.tau}): {el:.2f} s, "
+                               f"{res.n_compute}/{res.n_calls} calls computed")}
     m1 = dataclasses.replace(model_cfg, n_blocks=1)
     W = {k: v.astype(np.float64) for k, v in synth.unflatten(m1, synth.make_weights(m1)).items()}
     x = synth.make_noise(m1, 1)[0]
@@ -471,7 +494,10 @@ def main(argv=None):
         if budget.fits(60.0):
             progress("timing the CPU oracle on a sample")
             try:
-                cpu = cpu_baseline(m, computed / (N * steps_timed), nb)
+                wl_cpu = synth.Workload(wl.name, m, r, synth.make_weights(m, init=args.init), wl.ctx[:nb],
+                                        wl.noise, wl.scorer, wl.timesteps) \
+                    if eval_flop(m) * N * nb * T <= ORACLE_FULL_ROLLOUT_FLOP else None
+                cpu = cpu_baseline(m, computed / (N * steps_timed), nb, wl_cpu)
             except Exception as e:  # report, never hide
                 cpu = {"value": None, "error": repr(e)}
         else:

@@ -169,3 +169,13 @@ def test_decision_log_records(tmp_path):
     assert recs[5] == {"k": 2, "i": 0, "b": 1, "a": 0.2, "decision": "compute"}
     assert recs[6] == {"k": 2, "i": 1, "b": 0, "a": 0.07, "decision": "skip"}
     assert sum(r["decision"] == "skip" for r in recs) == 3
+
+
+def test_cpu_leg_runs_the_whole_oracle_rollout_only_for_small_workloads():
+    from paper_2607_23159_amd import synth
+    tiny = synth.MODELS["tiny"]
+    assert bench.eval_flop(tiny) * 4 * 10 <= bench.ORACLE_FULL_ROLLOUT_FLOP
+    for name in ("wan_mid", "wan13b", "wan5b"):
+        assert bench.eval_flop(synth.MODELS[name]) * 8 * 50 > bench.ORACLE_FULL_ROLLOUT_FLOP
+    # the 1.3B shape's per-call count used in the roofline analysis
+    assert bench.eval_flop(synth.MODELS["wan13b"]) == pytest.approx(2.83e14, rel=0.02)
