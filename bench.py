@@ -188,9 +188,9 @@ def parse(argv=None):
                    help="wall-clock budget from process start for all legs")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true", help="no per-kernel HIP event timing")
-    p.add_argument("--mode", choices=["adaptive", "static", "pab"], default="adaptive",
-                   help="reuse engine: the drift-indicator cache, the static schedule, or "
-                        "attention-output broadcasting")
+    p.add_argument("--mode", choices=["adaptive", "static", "pab", "off"], default=None,
+                   help="reuse engine: the drift-indicator cache, the static schedule, "
+                        "attention-output broadcasting, or none (default: the workload's own)")
     p.add_argument("--static-k", type=int, default=None, help="static schedule period")
     p.add_argument("--no-static-leg", action="store_true",
                    help="skip the static-schedule rollout at the headline's skip fraction")
@@ -332,8 +332,8 @@ def main(argv=None):
     dtype = synth.DTYPE_FP32 if args.fp32 else synth.DTYPE_BF16
     nb = 2 if args.cfg else 1
     t_gen = time.perf_counter()
-    mode = {"adaptive": synth.CACHE_ADAPTIVE, "static": synth.CACHE_STATIC,
-            "pab": synth.CACHE_PAB}[args.mode]
+    mode = None if args.mode is None else {"adaptive": synth.CACHE_ADAPTIVE, "static": synth.CACHE_STATIC,
+                                           "pab": synth.CACHE_PAB, "off": synth.CACHE_OFF}[args.mode]
     extra = {} if args.static_k is None else {"static_k": args.static_k}
     if args.k_warm is not None:
         extra["k_warm"] = args.k_warm
@@ -347,6 +347,7 @@ def main(argv=None):
                              pab_self=args.pab_self, pab_cross=args.pab_cross, **extra)
     m = wl.model
     r = dataclasses.replace(wl.roll, n_branch=nb)
+    mode = r.mode          # the engine actually run (workload default or --mode)
     gen_s = time.perf_counter() - t_gen
     progress(f"inputs generated ({gen_s:.1f} s); uploading weights")
     gm = GpuModel(m, wl.weights)
