@@ -60,14 +60,18 @@ struct alignas(16) Chunk16 { uint32_t w[4]; };
 CS_DEV Chunk16 ld16(const void* p) { return *reinterpret_cast<const Chunk16*>(p); }
 CS_DEV void st16(void* p, Chunk16 c) { *reinterpret_cast<Chunk16*>(p) = c; }
 
-// GELU, tanh form, with tanh(u) = 1 - 2 / (1 + 2^(2 u log2 e)) on the
-// hardware exp2 and reciprocal (saturates correctly to +-1 for large |u|).
+// GELU, tanh form: 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
+// Since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)), it is evaluated as
+// x / (1 + 2^(x (c1 + c3 x^2))) with c1 = -2 sqrt(2/pi) log2(e) and
+// c3 = 0.044715 c1: two multiplies and a multiply-add for the exponent, the
+// hardware exp2 and reciprocal, an add and a multiply (the tanh form took
+// twice the VALU work).  Large |x| saturate correctly: 2^(+big) = inf gives
+// x / inf = 0 for x < 0, 2^(-big) = 0 gives x for x > 0.
 CS_DEV float gelu_tanh(float x) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  const float u = k0 * (x + 0.044715f * x * x * x);
-  const float e = __builtin_amdgcn_exp2f(u * 2.8853900817779268f);  // e^(2u)
-  const float t = 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + e);
-  return 0.5f * x * (1.0f + t);
+  const float c1 = -2.302208198144325f;           // -2 sqrt(2/pi) / ln(2)
+  const float c3 = -0.1029432395800235f;          // 0.044715 * c1
+  const float z = x * fmaf(x * x, c3, c1);        // -2 u log2(e)
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
 }
 CS_DEV float silu(float x) { return x / (1.0f + expf(-x)); }
 
