@@ -196,6 +196,8 @@ def parse(argv=None):
                    help="skip the static-schedule rollout at the headline's skip fraction")
     p.add_argument("--init", choices=["paper", "stress"], default="paper",
                    help="weight init: the workload's N(0, 0.02), or the test-only stress init")
+    p.add_argument("--ctx-seed", type=int, default=1, help="seed of the conditional text context (a stand-in prompt)")
+    p.add_argument("--noise-seed0", type=int, default=100, help="noise seed of the first candidate")
     p.add_argument("--k-warm", type=int, default=None, help="forced warmup steps")
     p.add_argument("--k-cool", type=int, default=None, help="forced cooldown steps")
     p.add_argument("--decision-log", default=None,
@@ -344,7 +346,8 @@ def main(argv=None):
     want_cfg_leg = nb == 1 and not args.no_cfg_leg
     wl = synth.make_workload(args.workload, n_branch=2 if want_cfg_leg else nb, dtype=dtype, init=args.init,
                              n_cand=args.n_cand, n_steps=args.n_steps, tau=args.tau, mode=mode,
-                             pab_self=args.pab_self, pab_cross=args.pab_cross, **extra)
+                             pab_self=args.pab_self, pab_cross=args.pab_cross, ctx_seed=args.ctx_seed,
+                             noise_seed0=args.noise_seed0, **extra)
     m = wl.model
     r = dataclasses.replace(wl.roll, n_branch=nb)
     mode = r.mode          # the engine actually run (workload default or --mode)
@@ -620,7 +623,8 @@ def main(argv=None):
                                    + f", B={nb}, " + ("random init" if args.init == "paper"
                                                       else "stress init (test-only)")),
                    "n_cand": N, "n_steps": T, "tau": r.tau, "n_branch": nb,
-                   "cache_mode": r.mode},
+                   "cache_mode": r.mode, "init": args.init, "ctx_seed": args.ctx_seed,
+                   "noise_seed0": args.noise_seed0},
         "skip_fraction": round(1.0 - computed / max(calls, 1), 4),
         "n_compute_histogram": n_compute_histogram(masks),
         "attn_reuse_fraction": ({"self": round(reused[0] / max(calls, 1), 4),

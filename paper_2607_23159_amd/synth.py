@@ -314,7 +314,11 @@ def make_workload(name: str, *, n_branch: int = 1, dtype: Optional[int] = None,
                   init: str = "paper", n_cand: Optional[int] = None,
                   n_steps: Optional[int] = None, tau: Optional[float] = None,
                   mode: Optional[int] = None, model: Optional[str] = None,
+                  ctx_seed: int = CTX_COND_SEED, noise_seed0: int = NOISE_SEED0,
                   **roll_overrides) -> Workload:
+    """A workload by name.  ``ctx_seed`` draws the conditional text context
+    (a stand-in prompt; the unconditional one keeps its own seed) and
+    ``noise_seed0`` the first candidate's noise seed."""
     mname, roll = WORKLOADS[name] if name in WORKLOADS else (name, RolloutCfg(1, 10))
     if model is not None:
         mname = model
@@ -331,10 +335,10 @@ def make_workload(name: str, *, n_branch: int = 1, dtype: Optional[int] = None,
     if mode is not None:
         kw["mode"] = mode
     roll = dataclasses.replace(roll, **kw)
-    ctx = [make_context(m, CTX_COND_SEED)]
+    ctx = [make_context(m, ctx_seed)]
     if roll.n_branch == 2:
         ctx.append(make_context(m, CTX_UNCOND_SEED))
     return Workload(name=name, model=m, roll=roll,
                     weights=make_weights(m, init=init), ctx=ctx,
-                    noise=make_noise(m, roll.n_cand), scorer=make_scorer(m),
+                    noise=make_noise(m, roll.n_cand, noise_seed0), scorer=make_scorer(m),
                     timesteps=timestep_grid(roll.n_steps, roll.shift))
