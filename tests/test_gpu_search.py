@@ -93,6 +93,57 @@ def test_single_candidate_rollout_and_batch_invariance_of_rollouts():
     gm.close()
 
 
+def test_maximum_candidate_count():
+    """N = 1024 seeds (the largest the library accepts) with two guidance
+    branches: 2048 streams, the decision kernel's capacity.  Cache on, tiny
+    model in fp32.  Sampled candidates equal their single-candidate rollouts
+    bit for bit and follow the oracle's schedule, latents and score; the
+    library's order of all 1024 scores is the descending sort; N = 0 and
+    N = 1025 are rejected before any device work."""
+    N = 1024
+    wl = synth.make_workload("tiny", n_branch=2, init="stress", dtype=synth.DTYPE_FP32, n_cand=N)
+    assert wl.noise.shape[0] == N and wl.roll.n_cand == N
+    T, tau = wl.roll.n_steps, wl.roll.tau
+    gm = GpuModel(wl.model, wl.weights)
+    inp = Inputs(wl)
+    g = run_rollout(gm, wl, inp)
+    say(f"N={N}: computed {g.computed} of {g.calls} calls; per-step n_compute "
+        f"{g.masks.sum(axis=1).tolist()}")
+    assert g.calls == T * 2 * N
+    D = int(wl.noise[0].size)
+    w_norm = float(np.linalg.norm(wl.scorer.astype(np.float64)))
+    for i in (0, 517, N - 1):
+        one = synth.Workload(wl.name, wl.model, wl.roll, wl.weights, wl.ctx, wl.noise[i:i + 1], wl.scorer,
+                             wl.timesteps)
+        g1 = run_rollout(gm, one, n_cand=1)
+        assert np.array_equal(g1.masks, g.masks[:, 2 * i:2 * i + 2]), f"candidate {i}: schedule differs alone"
+        assert np.array_equal(g1.latents[0], g.latents[i]), f"candidate {i}: latent differs alone"
+        assert g1.scores[0] == g.scores[i]
+        if i == 517:
+            continue
+        res = orl.run_workload(one)
+        om, oa = oracle_masks(res, 1, 2, T)
+        exc = compare_schedules(g1.masks, om, oa, tau)
+        lat = run_rollout(gm, one, n_cand=1, override=om).latents[0] if exc else g1.latents[0]
+        err = rel_l2(lat, res.latents[0])
+        s_ref = float(orl.score(res.latents, wl.scorer)[0])
+        # the score is linear in the latent: |s - s_ref| <= |w| |x - x_ref| / sqrt(D)
+        dx = float(np.linalg.norm((g1.latents[0].astype(np.float64) - res.latents[0]).ravel()))
+        bound = w_norm * dx / math.sqrt(D) * (1 + 1e-6) + 1e-9
+        say(f"  candidate {i}: excused {exc}, rel_l2 {err:.3e}, score {g1.scores[0]:.6f} vs oracle "
+            f"{s_ref:.6f} (bound {bound:.2e})")
+        assert err < TOL[synth.DTYPE_FP32]
+        assert abs(g1.scores[0] - s_ref) <= bound
+    order, _, _, _ = B.cs_rank(g.scores, None)
+    assert order == np.argsort(-np.asarray(g.scores, np.float64), kind="stable").tolist()
+    for n_bad, x in ((0, torch.empty(0, device="cuda")), (N + 1, torch.zeros((N + 1) * D, device="cuda"))):
+        with pytest.raises(B.CsError) as e:
+            B.cs_rollout_init(gm.h, B.RolloutDesc(wl.roll, wl.timesteps, n_cand=n_bad), x, inp.ctx[0],
+                              inp.ctx[1])
+        assert e.value.status == B.CS_E_INVAL and "n_cand" in str(e.value)
+    gm.close()
+
+
 def test_state_machine_errors():
     wl = synth.make_workload("tiny", dtype=synth.DTYPE_FP32, init="stress")
     gm = GpuModel(wl.model, wl.weights)
