@@ -323,6 +323,35 @@ def test_static_mode_schedule():
         assert rel_l2(g.latents[i], res.latents[i]) < TOL[1]
 
 
+def test_degenerate_schedules():
+    """Degenerate settings of the skip rule (Sec. Method, adaptive skip rule
+    and its static variant): the static period 1 computes every call and the
+    literal warmup and cooldown windows K_w = K_c = 5 at T = 10 force every
+    call even at tau = inf, both bitwise equal to the uncached rollout; a
+    one-step rollout (T = 1, its only call forced) matches the oracle."""
+    gm, m = gpu_model("tiny", synth.DTYPE_BF16, "stress")
+    wl = workload("tiny", 2, "stress", synth.DTYPE_BF16)
+    off = run_rollout(gm, wl, mode=synth.CACHE_OFF)
+    st1 = synth.make_workload("tiny", n_branch=2, dtype=synth.DTYPE_BF16, init="stress",
+                              mode=synth.CACHE_STATIC, static_k=1)
+    for w, kw in ((st1, {}), (synth.make_workload("tiny", n_branch=2, dtype=synth.DTYPE_BF16, init="stress",
+                                                  k_warm=5, k_cool=5), {"tau": math.inf})):
+        g = run_rollout(gm, w, **kw)
+        assert g.computed == g.calls == off.calls
+        assert np.array_equal(g.latents, off.latents) and np.array_equal(g.scores, off.scores)
+    for dtype in (synth.DTYPE_FP32, synth.DTYPE_BF16):
+        gm1, _ = gpu_model("tiny", dtype, "stress")
+        one = synth.make_workload("tiny", n_branch=2, dtype=dtype, init="stress", n_steps=1)
+        assert list(one.timesteps) == [1.0, 0.0]
+        g = run_rollout(gm1, one)
+        assert g.masks.shape == (1, 2 * one.roll.n_cand) and g.masks.all()
+        res = orl.run_workload(one)
+        for i in range(one.roll.n_cand):
+            err = rel_l2(g.latents[i], res.latents[i])
+            say(f"  T=1 dtype={dtype} i={i} rel_l2={err:.3e}")
+            assert err < TOL[dtype]
+
+
 def test_replay_override_follows_given_schedule():
     gm, m = gpu_model("tiny", synth.DTYPE_FP32, "stress")
     wl = workload("tiny", 1, "stress", synth.DTYPE_FP32)
