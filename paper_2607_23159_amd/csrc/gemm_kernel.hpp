@@ -548,9 +548,10 @@ CS_DEV void gemm_epilogue16_deep(const f32x4 (&acc)[TM][TN], int row_base, int c
 // Same LDS row layout, tiled weights, tile order and accumulation order over
 // K as k_gemm_dl: results are bitwise equal to it.
 // ---------------------------------------------------------------------------
-// Epilogues that write some tiles transposed route those tiles through LDS
-// (store_transposed_tile), after the main loop has released it.
-template <class Epi> struct EpiTransposesTiles : std::false_type {};
+// Epilogues that route a workgroup's tile through LDS on its way out
+// (staged_tile / store_staged_tile), once the main loop has released the
+// ring: each wave gets a region of max(WN (WM + 8), WM (WN + 8)) elements.
+template <class Epi> struct EpiStagesTiles : std::false_type {};
 
 CS_DEV void mfma_16x16x32_agpr(f32x4& acc, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
@@ -722,11 +723,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm_w4(const bf16* __restrict__ A, 
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) asm volatile("" : "+a"(acc[i][j]));  // read only after the nops
-  if constexpr (EpiTransposesTiles<Epi>::value) {
-    static_assert(NWAVE * WN * (WM + 8) <= 3 * A_BUF + 2 * B_BUF, "transpose staging fits the ring");
-    if (epi.transposed_tile(n0)) {   // uniform over the workgroup
-      __syncthreads();               // every wave's last fragment reads are done
-      epi.store_transposed_tile(acc, smem + wave * WN * (WM + 8), m0 + wm * WM, n0 + wn * WN, lane, M, N);
+  if constexpr (EpiStagesTiles<Epi>::value) {
+    constexpr int STG = WN * (WM + 8) > WM * (WN + 8) ? WN * (WM + 8) : WM * (WN + 8);
+    static_assert(NWAVE * STG <= 3 * A_BUF + 2 * B_BUF, "staging fits the ring");
+    if (epi.staged_tile(n0)) {   // uniform over the workgroup
+      __syncthreads();           // every wave's last fragment reads are done
+      epi.store_staged_tile(acc, smem + wave * STG, m0 + wm * WM, n0 + wn * WN, lane, M, N);
       return;
     }
   }
@@ -749,6 +751,54 @@ template <typename T> CS_DEV void store4(T* p, const float* y) {
 }
 struct NoPre {};
 
+// Row-major bf16 store of one wave's TM*16 x TN*16 block of 16x16
+// accumulators (lane holds row row_base + 16i + (lane & 15), columns
+// col_base + 16j + 4(lane >> 4) + r) through `stage` (TM*16 rows of TN*16 + 8
+// elements): written as 8-byte pieces, read back and stored as 16-byte runs,
+// 256 contiguous bytes per row, where the direct path stores 32-byte pieces
+// of 16 rows per instruction.  f maps each value before its rounding.
+// Contains one workgroup barrier: every wave of the workgroup calls a staged
+// store exactly once.
+template <int TM, int TN, class F>
+CS_DEV void store_rows_staged(const f32x4 (&acc)[TM][TN], bf16* stage, int row_base, int col_base,
+                              int lane, int M, int N, bf16* out, long ldo, F f) {
+  constexpr int R = TM * 16, C = TN * 16, SP = C + 8;
+  constexpr int LPR = C / 8, RPI = 64 / LPR;   // lanes per row, rows per instruction
+  static_assert(64 % LPR == 0 && R % RPI == 0, "readback split");
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      bf16x4 q;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) q[r] = (bf16)f(acc[i][j][r]);
+      *reinterpret_cast<bf16x4*>(stage + (16 * i + (lane & 15)) * SP + 16 * j + 4 * (lane >> 4)) = q;
+    }
+  __syncthreads();
+  const int c = 8 * (lane % LPR), col = col_base + c;
+  const bool whole = col + 8 <= N && ((ldo | col) & 7) == 0;
+#pragma unroll 4
+  for (int q = 0; q < R / RPI; ++q) {
+    const int r = RPI * q + lane / LPR, row = row_base + r;
+    if (row >= M) continue;
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(stage + r * SP + c);
+    bf16* dst = out + (long)row * ldo + col;
+    if (whole && ((uintptr_t)dst & 15) == 0) {
+      *reinterpret_cast<bf16x8*>(dst) = v;
+    } else {
+      for (int e = 0; e < 8 && col + e < N; ++e) dst[e] = v[e];
+    }
+  }
+}
+
+struct IdentityF { CS_DEV float operator()(float x) const { return x; } };
+struct GeluF { CS_DEV float operator()(float x) const { return gelu_tanh(x); } };
+
+// On the bf16 kernel every tile goes out through LDS (store_rows_staged).
+// Measured against the element-wise path at 8 x 32,760 rows, d = 1536, same
+// process: cross q (N = 1536) 1.036 -> 0.938 ms, q|k (N = 3072) 2.032 ->
+// 1.895 ms, FFN up + GELU (N = 8960) unchanged (5.877 vs 5.886 ms); same
+// values.
 template <typename T, int ACT> struct EpiStore {  // ACT: 0 none, 1 tanh-GELU
   T* out; long ldo; const float* bias;
   typedef NoPre Pre;
@@ -761,19 +811,33 @@ template <typename T, int ACT> struct EpiStore {  // ACT: 0 none, 1 tanh-GELU
     }
     store4<T>(out + (long)row * ldo + col0, y);
   }
+
+  CS_DEV bool staged_tile(int) const { return true; }
+  template <int TM, int TN>
+  CS_DEV void store_staged_tile(const f32x4 (&acc)[TM][TN], bf16* stage, int row_base, int col_base,
+                                int lane, int M, int N) const {
+    static_assert(sizeof(T) == 2, "bf16 tiles only");
+    if constexpr (ACT == 1)
+      store_rows_staged(acc, stage, row_base, col_base, lane, M, N, out, ldo, GeluF{});
+    else
+      store_rows_staged(acc, stage, row_base, col_base, lane, M, N, out, ldo, IdentityF{});
+  }
 };
+template <int ACT> struct EpiStagesTiles<EpiStore<bf16, ACT>> : std::true_type {};
 
 // Self-attention projection: columns [0, 2d) are q and k, stored row-major
 // [row][2d]; columns [2d, 3d) are v, stored transposed per stream as
 // vT[stream][channel][token] with a padded token stride.
 //
-// On the bf16 kernel a workgroup whose 256 columns all lie in v transposes
-// its tile through LDS: each wave writes its 128 x 128 block there as
-// [channel][token] (token stride 136, 16-byte aligned rows) and stores it
+// On the bf16 kernel every tile goes out through LDS.  A wave whose 128
+// columns lie in v (2d is a multiple of 128) writes its 128 x 128 block there
+// as [channel][token] (token stride 136, 16-byte aligned rows) and stores it
 // back as 16-byte runs of 8 tokens, 256 contiguous bytes per channel, where
 // the element-wise path below issues a 2-byte store per value (measured: the
-// QKV projection 3.386 -> 3.167 ms at 8 x 32,760 rows, d = 1536, within 0.5%
-// of storing v row-major; bitwise equal).
+// v part alone: 3.386 -> 3.167 ms for the QKV projection at 8 x 32,760 rows,
+// d = 1536, within 0.5% of storing v row-major); a wave in q|k stores its
+// rows through store_rows_staged (both parts staged: 3.203 -> 2.886 ms;
+// bitwise equal).
 template <typename T> struct EpiQKV {
   T* qk; T* vt; const float* bias; int d; int L; long vt_ld; long vt_ss;
   typedef NoPre Pre;
@@ -789,15 +853,25 @@ template <typename T> struct EpiQKV {
     }
   }
 
-  CS_DEV bool transposed_tile(int n0) const { return n0 >= 2 * d; }
+  CS_DEV bool staged_tile(int) const { return true; }
+
+  template <int TM, int TN>
+  CS_DEV void store_staged_tile(const f32x4 (&acc)[TM][TN], bf16* stage, int row_base, int col_base,
+                                int lane, int M, int N) const {
+    static_assert(sizeof(T) == 2, "bf16 tiles only");
+    if (col_base >= 2 * d)
+      store_v_transposed(acc, stage, row_base, col_base, lane, M, N);
+    else
+      store_rows_staged(acc, stage, row_base, col_base, lane, M, 2 * d, qk, 2L * d, IdentityF{});
+  }
 
   // One wave's TM*16 x TN*16 block of 16x16 accumulators (lane holds row
   // row_base + 16i + (lane & 15), columns col_base + 16j + 4(lane >> 4) + r)
-  // through `stage` (TN*16 rows of TM*16 + 8 tokens) to vT.
+  // through `stage` (TN*16 rows of TM*16 + 8 tokens) to vT; one workgroup
+  // barrier, like store_rows_staged.
   template <int TM, int TN>
-  CS_DEV void store_transposed_tile(const f32x4 (&acc)[TM][TN], bf16* stage, int row_base,
-                                    int col_base, int lane, int M, int N) const {
-    static_assert(sizeof(T) == 2, "bf16 tiles only");
+  CS_DEV void store_v_transposed(const f32x4 (&acc)[TM][TN], bf16* stage, int row_base,
+                                 int col_base, int lane, int M, int N) const {
     constexpr int R = TM * 16, C = TN * 16, SP = R + 8, CHUNKS = R / 8;
     static_assert(64 % CHUNKS == 0 && C % (64 / CHUNKS) == 0, "readback split");
 #pragma unroll
@@ -835,7 +909,7 @@ template <typename T> struct EpiQKV {
     }
   }
 };
-template <> struct EpiTransposesTiles<EpiQKV<bf16>> : std::true_type {};
+template <> struct EpiStagesTiles<EpiQKV<bf16>> : std::true_type {};
 
 // Transposed store of a single-stream projection: out[col][row].
 template <typename T> struct EpiStoreT {
