@@ -128,6 +128,19 @@ def leg_estimates(rollout_s: float, computed: int, n_cand: int, n_steps: int, n_
     }
 
 
+def cost_model(cc: float, cf: float, n: int) -> dict:
+    """Search costs from the per-candidate cached and full rollout costs C_c,
+    C_f (Sec. Method, cost analysis, Eq. costs): keep = N C_c, commit =
+    N C_c + C_f, best-of-N = N C_f; gamma = C_c / C_f and the break-even
+    width N* = 1 / (1 - gamma) beyond which commit is cheaper than best-of-N
+    (Eq. breakeven)."""
+    gamma = cc / cf
+    return {"C_c_s": round(cc, 3), "C_f_s": round(cf, 3), "gamma": round(gamma, 4),
+            "break_even_N": round(1.0 / (1.0 - gamma), 3) if gamma < 1 else None,
+            "keep_s": round(n * cc, 2), "commit_s": round(n * cc + cf, 2),
+            "best_of_N_full_s": round(n * cf, 2)}
+
+
 def static_computes(n_steps: int, k_warm: int, k_cool: int, period: int) -> int:
     """Computed steps per stream of the static schedule (the uniform baseline
     of Sec. Method, properties): the forced windows, the first step (no
@@ -538,13 +551,7 @@ def main(argv=None):
 
     costs = None
     if full_s is not None:
-        cc = rollout_s / N
-        cf = full_s / N
-        gamma = cc / cf
-        costs = {"C_c_s": round(cc, 3), "C_f_s": round(cf, 3), "gamma": round(gamma, 4),
-                 "break_even_N": round(1.0 / (1.0 - gamma), 3) if gamma < 1 else None,
-                 "keep_s": round(N * cc, 2), "commit_s": round(N * cc + cf, 2),
-                 "best_of_N_full_s": round(N * cf, 2)}
+        costs = cost_model(rollout_s / N, full_s / N, N)
 
     # ---- guided rollout (B = 2, w = 5): both branches evaluated per step
     cfg_rec = None

@@ -179,3 +179,28 @@ def test_cpu_leg_runs_the_whole_oracle_rollout_only_for_small_workloads():
         assert bench.eval_flop(synth.MODELS[name]) * 8 * 50 > bench.ORACLE_FULL_ROLLOUT_FLOP
     # the 1.3B shape's per-call count used in the roofline analysis
     assert bench.eval_flop(synth.MODELS["wan13b"]) == pytest.approx(2.83e14, rel=0.02)
+
+
+def test_cost_model_reproduces_the_papers_worked_example():
+    """The cost model (Eqs. costs and breakeven) applied to the per-rollout
+    costs the paper measures gives its printed search costs at N = 4 and 8,
+    the cost fractions of best-of-N, gamma and the break-even width
+    (tests/golden/cost_model_wan13b.json, with its citation)."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "cost_model_wan13b.json")))
+    for row in g["rows"]:
+        c = bench.cost_model(g["C_c_s"], g["C_f_s"], row["N"])
+        for key, printed in (("best_of_N_full_s", row["best_of_N_s"]), ("keep_s", row["keep_s"]),
+                             ("commit_s", row["commit_s"])):
+            assert abs(c[key] - printed) <= 0.005 * printed, (row["N"], key, c[key], printed)
+        assert abs(c["keep_s"] / c["best_of_N_full_s"] - row["keep_frac"]) <= 0.0015
+        assert abs(c["commit_s"] / c["best_of_N_full_s"] - row["commit_frac"]) <= 0.0015
+        assert abs(c["gamma"] - g["gamma"]) <= 0.005
+        assert abs(c["break_even_N"] - g["break_even_N"]) <= 0.005
+    # commit beats best-of-N exactly beyond the break-even width
+    c = bench.cost_model(g["C_c_s"], g["C_f_s"], 2)
+    assert c["commit_s"] > c["best_of_N_full_s"]
+    c = bench.cost_model(g["C_c_s"], g["C_f_s"], 3)
+    assert c["commit_s"] < c["best_of_N_full_s"]
+    assert bench.cost_model(5.0, 5.0, 4)["break_even_N"] is None
