@@ -135,10 +135,10 @@ def cost_model(cc: float, cf: float, n: int) -> dict:
     width N* = 1 / (1 - gamma) beyond which commit is cheaper than best-of-N
     (Eq. breakeven)."""
     gamma = cc / cf
-    return {"C_c_s": round(cc, 3), "C_f_s": round(cf, 3), "gamma": round(gamma, 4),
+    sig = lambda x: float(f"{x:.4g}")   # seconds to 4 significant digits (tiny workloads take ms)
+    return {"C_c_s": sig(cc), "C_f_s": sig(cf), "gamma": round(gamma, 4),
             "break_even_N": round(1.0 / (1.0 - gamma), 3) if gamma < 1 else None,
-            "keep_s": round(n * cc, 2), "commit_s": round(n * cc + cf, 2),
-            "best_of_N_full_s": round(n * cf, 2)}
+            "keep_s": sig(n * cc), "commit_s": sig(n * cc + cf), "best_of_N_full_s": sig(n * cf)}
 
 
 def static_computes(n_steps: int, k_warm: int, k_cool: int, period: int) -> int:
